@@ -1,0 +1,362 @@
+"""Plain CPU fp64 oracle of the Token Radius Attention (TRA) hot path.
+
+TEST INFRASTRUCTURE.  Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import or run this module.  The GPU library never calls
+it, and it shares no code, table or helper with the library: every quantity
+here is recomputed from the paper's definitions.
+
+Precision: all floating-point work is fp64 (numpy, and torch CPU ops in
+float64 for the large matrix products, softmax and exponentials).  Integer
+geometry is numpy int64.
+
+Conventions
+-----------
+* Raster token index i = (f*H + x)*W + y on an F x H x W latent grid
+  (Sec. 2.1: a token carries a coordinate (f, x, y)).
+* Tensors per head are (N, d) in raster order.
+* "FULL" radius (the full-support candidate radius of Sec. 3.2) is returned as
+  ``RADIUS_FULL`` (2**31 - 1), matching the library's sentinel value, and is
+  treated as an infinite radius.
+
+Readings of the paper this oracle takes where the paper is silent are listed in
+the design notes; each function below names the passage it follows.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+RADIUS_FULL = 2 ** 31 - 1
+
+__all__ = [
+    "RADIUS_FULL", "grid_coords", "tile_major_order", "block_bounds",
+    "scores", "softmax_rows", "dense_attention", "entropy_from_probs",
+    "entropy_online", "token_budget", "n_cap", "threshold_table",
+    "within_radius", "grid_count_bruteforce", "disk_count_table", "grid_count",
+    "select_radius", "select_radius_linear", "token_mask_rows",
+    "block_mask_rows", "masked_attention_rows", "retained_fraction",
+    "top_tau_support", "analytic_radius",
+]
+
+
+# ============================================================ geometry, layout
+def grid_coords(F: int, H: int, W: int):
+    """(f, x, y) of every raster token (Sec. 2.1)."""
+    i = np.arange(F * H * W, dtype=np.int64)
+    return i // (H * W), (i // W) % H, i % W
+
+
+def tile_major_order(F: int, H: int, W: int, tile_h: int, tile_w: int) -> np.ndarray:
+    """Tile-major token order (Sec. 3.3, "Flash Radius Mask Kernel"; App. C.1,
+    "Kernel execution").
+
+    Each H x W frame is cut into tile_h x tile_w tiles (edge tiles clipped, not
+    padded); tokens are listed frame by frame, tile row by tile row, tile by
+    tile, and row-major inside a tile.  Returns perm with perm[p] = raster index
+    of the token at tile-major position p.
+    """
+    frame = []
+    for ty in range(0, H, tile_h):
+        for tx in range(0, W, tile_w):
+            for x in range(ty, min(H, ty + tile_h)):
+                for y in range(tx, min(W, tx + tile_w)):
+                    frame.append(x * W + y)
+    frame = np.asarray(frame, dtype=np.int64)
+    return np.concatenate([f * H * W + frame for f in range(F)])
+
+
+def block_bounds(N: int, b: int):
+    """Block u holds tile-major positions [u*b, min((u+1)*b, N)) (App. C:
+    B = ceil(S/b) blocks of b tokens)."""
+    nb = -(-N // b)
+    return [(u * b, min((u + 1) * b, N)) for u in range(nb)]
+
+
+# ===================================================== attention and entropy
+def _t(x):
+    return torch.as_tensor(np.asarray(x, dtype=np.float64))
+
+
+def scores(q, k):
+    """s_ij = q_i . k_j / sqrt(d) (Sec. 2.1, Eq. 1), fp64."""
+    q, k = _t(q), _t(k)
+    return (q @ k.T) / math.sqrt(q.shape[1])
+
+
+def softmax_rows(s):
+    """p_ij = exp(s_ij) / sum_n exp(s_in) (Eq. 1); entries at -inf get 0."""
+    s = _t(s) if not isinstance(s, torch.Tensor) else s
+    m = s.max(dim=1, keepdim=True).values
+    e = torch.exp(s - m)
+    return e / e.sum(dim=1, keepdim=True)
+
+
+def dense_attention(q, k, v, return_probs=False):
+    """o_i = sum_j p_ij v_j (Eq. 1).  q: (R, d) rows, k, v: (N, d)."""
+    p = softmax_rows(scores(q, k))
+    o = p @ _t(v)
+    return (o.numpy(), p) if return_probs else o.numpy()
+
+
+def entropy_from_probs(p) -> np.ndarray:
+    """H_i = -sum_j p_ij log p_ij in nats, with 0 log 0 = 0 (Sec. 2.2, Eq. 2)."""
+    p = p if isinstance(p, torch.Tensor) else _t(p)
+    safe = torch.where(p > 0, p, torch.ones_like(p))
+    return (-(p * torch.log(safe)).sum(dim=1)).numpy()
+
+
+def entropy_online(q, k, v, kv_tile: int):
+    """Alg. 2 (App. C.2): online softmax with one extra running sum.
+
+    Per query row: m = -inf, l = 0, a = 0, o = 0; for each KV tile r:
+    s = alpha q K_r^T, m_r = max s, w = exp(s - m_r), l_r = sum w,
+    a_r = sum w s, o_r = sum w v; m' = max(m, m_r); u = exp(m - m');
+    v' = exp(m_r - m'); l = u l + v' l_r; a = u a + v' a_r; o = u o + v' o_r;
+    m = m'.  Finally O = o / l and H = log l + m - a / l, which is the identity
+    H = log Z - sum_j p_ij s_ij of App. C.2.
+    Returns (O, H) for all rows of q.
+    """
+    q, k, v = _t(q), _t(k), _t(v)
+    R, d = q.shape
+    alpha = 1.0 / math.sqrt(d)
+    m = torch.full((R,), -math.inf, dtype=torch.float64)
+    l = torch.zeros(R, dtype=torch.float64)
+    a = torch.zeros(R, dtype=torch.float64)
+    o = torch.zeros(R, v.shape[1], dtype=torch.float64)
+    for s0 in range(0, k.shape[0], kv_tile):
+        kr, vr = k[s0:s0 + kv_tile], v[s0:s0 + kv_tile]
+        s = alpha * (q @ kr.T)
+        m_r = s.max(dim=1).values
+        w = torch.exp(s - m_r[:, None])
+        l_r = w.sum(dim=1)
+        a_r = (w * s).sum(dim=1)
+        o_r = w @ vr
+        m_new = torch.maximum(m, m_r)
+        u = torch.exp(m - m_new)
+        vv = torch.exp(m_r - m_new)
+        l = u * l + vv * l_r
+        a = u * a + vv * a_r
+        o = u[:, None] * o + vv[:, None] * o_r
+        m = m_new
+    return (o / l[:, None]).numpy(), (torch.log(l) + m - a / l).numpy()
+
+
+# ====================================================== entropy -> budget
+def token_budget(H, tau: float, N: int) -> np.ndarray:
+    """K_hat = ceil(tau * exp(H)) (Sec. 3.1, Eq. 8; App. C.1,
+    Eq. implementation-budget-radius), in fp64, clamped to the key count
+    range [1, N] (a budget outside it has no meaning)."""
+    H = np.asarray(H, dtype=np.float64)
+    k = np.ceil(tau * np.exp(H))
+    return np.clip(k, 1, N).astype(np.int64)
+
+
+# ====================================================== budget -> radius
+def n_cap(H: int, W: int) -> int:
+    """Largest squared in-frame distance (H-1)^2 + (W-1)^2: beyond it a disk
+    covers its whole frame, so candidate squared radii stop there."""
+    return (H - 1) ** 2 + (W - 1) ** 2
+
+
+def threshold_table(ncap: int, F: int, gamma: float) -> np.ndarray:
+    """thr[n, delta] = floor(n * exp(-2 gamma delta)), n in [0, ncap], delta in [0, F).
+
+    For a squared base radius n (r = sqrt n) and an integer squared spatial
+    distance D, the test d_s <= r phi(delta) of Eq. 15 with phi = exp(-gamma
+    delta) (Eq. 10) is D <= n exp(-2 gamma delta), i.e. D <= thr[n, delta]."""
+    n = np.arange(ncap + 1, dtype=np.float64)[:, None]
+    delta = np.arange(F, dtype=np.float64)[None, :]
+    return np.floor(n * np.exp(-2.0 * gamma * delta)).astype(np.int64)
+
+
+def within_radius(D, n, delta, gamma: float):
+    """Eq. 15 literally, in fp64: sqrt(D) <= sqrt(n) * exp(-gamma * delta),
+    with the FULL radius treated as infinite (keeps every key)."""
+    D = np.asarray(D, dtype=np.float64)
+    n = np.asarray(n)
+    r = np.where(n == RADIUS_FULL, np.inf, np.sqrt(n.astype(np.float64)))
+    with np.errstate(invalid="ignore"):
+        rho = r * np.exp(-gamma * np.asarray(delta, dtype=np.float64))
+    return np.sqrt(D) <= rho
+
+
+def grid_count_bruteforce(i: int, n: int, F: int, H: int, W: int, gamma: float) -> int:
+    """C_i^grid(r) of Sec. 3.2, Eq. 13, by checking every key j against Eq. 15."""
+    f, x, y = grid_coords(F, H, W)
+    D = (x - x[i]) ** 2 + (y - y[i]) ** 2
+    return int(within_radius(D, n, np.abs(f - f[i]), gamma).sum())
+
+
+def disk_count_table(H: int, W: int, tmax: int) -> np.ndarray:
+    """disk[x, y, T] = #{(x', y') in the H x W frame : (x-x')^2 + (y-y')^2 <= T},
+    T in [0, tmax].  The per-frame lattice count of Eq. 13."""
+    xs, ys = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    xs, ys = xs.ravel(), ys.ravel()
+    out = np.empty((H, W, tmax + 1), dtype=np.int64)
+    for x in range(H):
+        for y in range(W):
+            D = (xs - x) ** 2 + (ys - y) ** 2
+            out[x, y] = np.cumsum(np.bincount(D, minlength=tmax + 1)[: tmax + 1])
+    return out
+
+
+def grid_count(f, x, y, n, F: int, thr: np.ndarray, disk: np.ndarray) -> np.ndarray:
+    """C_i^grid for arrays of queries (f, x, y) and squared radii n (Eq. 13):
+    sum over frames t of the lattice points of frame t inside the disk of
+    squared radius thr[n, |t - f|].  n == FULL counts every key."""
+    f, x, y, n = (np.asarray(a, dtype=np.int64) for a in (f, x, y, n))
+    H, W, T1 = disk.shape
+    full = n == RADIUS_FULL
+    nn = np.where(full, 0, n)
+    total = np.zeros(f.shape, dtype=np.int64)
+    for t in range(F):
+        T = np.minimum(thr[nn, np.abs(t - f)], T1 - 1)
+        total += disk[x, y, T]
+    return np.where(full, F * H * W, total)
+
+
+def select_radius_linear(khat: int, i: int, F: int, H: int, W: int, gamma: float) -> int:
+    """r_i = min{r in R : C_i^grid(r) >= K_hat} (Sec. 3.2, Eq. 14) by scanning
+    every candidate squared radius n = 0, 1, ..., n_cap in order, counting by
+    brute force; the full-support radius if none reaches K_hat."""
+    for n in range(n_cap(H, W) + 1):
+        if grid_count_bruteforce(i, n, F, H, W, gamma) >= khat:
+            return n
+    return RADIUS_FULL
+
+
+def select_radius(khat, f, x, y, F: int, thr: np.ndarray, disk: np.ndarray) -> np.ndarray:
+    """Eq. 14 for arrays of queries: the smallest n in [0, n_cap] with
+    C_i^grid(n) >= K_hat, else FULL.  C_i^grid is non-decreasing in n (a larger
+    disk contains a smaller one), so the minimum is found by bisection."""
+    khat = np.asarray(khat, dtype=np.int64)
+    ncap = thr.shape[0] - 1
+    lo = np.zeros(khat.shape, dtype=np.int64)
+    hi = np.full(khat.shape, ncap, dtype=np.int64)
+    ok_at_cap = grid_count(f, x, y, hi, F, thr, disk) >= khat
+    while True:
+        active = lo < hi
+        if not active.any():
+            break
+        mid = (lo + hi) // 2
+        ge = grid_count(f, x, y, mid, F, thr, disk) >= khat
+        hi = np.where(active & ge, mid, hi)
+        lo = np.where(active & ~ge, mid + 1, lo)
+    return np.where(ok_at_cap, lo, RADIUS_FULL)
+
+
+def analytic_radius(khat, f, F: int, gamma: float) -> np.ndarray:
+    """Continuous initialisation r~ = sqrt(K_hat / (pi * sum_t phi^2)) of
+    Sec. 3.2, Eq. 12 (boundaries and lattice effects ignored)."""
+    t = np.arange(F)[None, :]
+    s = np.exp(-2.0 * gamma * np.abs(t - np.asarray(f)[:, None])).sum(axis=1)
+    return np.sqrt(np.asarray(khat, dtype=np.float64) / (math.pi * s))
+
+
+# ====================================================== radius -> masks
+def token_mask_rows(rows, n_rows, F: int, H: int, W: int, gamma: float, keys=None):
+    """M_ij = [d_s(i, j) <= r_i phi(|f_j - f_i|)] (Sec. 3.2, Eq. 15) for query
+    rows ``rows`` (raster indices) with squared radii ``n_rows``, against keys
+    ``keys`` (raster indices, default all).  Returns a bool torch tensor."""
+    f, x, y = grid_coords(F, H, W)
+    rows = np.asarray(rows, dtype=np.int64)
+    keys = np.arange(F * H * W) if keys is None else np.asarray(keys, dtype=np.int64)
+    fr, xr, yr = (torch.as_tensor(a[rows])[:, None] for a in (f, x, y))
+    fk, xk, yk = (torch.as_tensor(a[keys])[None, :] for a in (f, x, y))
+    D = ((xr - xk) ** 2 + (yr - yk) ** 2).to(torch.float64)
+    delta = (fr - fk).abs().to(torch.float64)
+    n = torch.as_tensor(np.asarray(n_rows, dtype=np.int64))
+    r = torch.where(n == RADIUS_FULL, torch.tensor(math.inf, dtype=torch.float64),
+                    torch.sqrt(n.to(torch.float64)))[:, None]
+    return torch.sqrt(D) <= r * torch.exp(-gamma * delta)
+
+
+def block_mask_rows(n_raster, perm, b: int, F: int, H: int, W: int, gamma: float,
+                    blocks, rule: str = "vote"):
+    """Block-mask rows M[u, :] of Alg. 1 (App. C.1) for the query blocks
+    ``blocks``, from per-token squared radii ``n_raster`` (raster order).
+
+    For a query block u and key block v (tile-major positions), every valid key
+    column j of v gets the count c_j of valid queries i of u with M_ij = 1
+    (Eq. 15).  C = {j : c_j > 0}, C_hi = {j : c_j > n_u / 3}.
+    vote:  retained iff |C| > 0 and 10 |C_hi| > 6 |C|   (Alg. 1);
+    union: retained iff |C| > 0.
+    The diagonal block (u, u) is always retained (every query keeps its own key).
+    n_u is the number of valid queries of u, which equals b except for the last
+    block; the high-coverage test is written 3 c_j > n_u.
+    Returns a bool array (len(blocks), NB).
+    """
+    perm = np.asarray(perm, dtype=np.int64)
+    N = perm.shape[0]
+    nb = -(-N // b)
+    out = np.zeros((len(blocks), nb), dtype=bool)
+    pad = nb * b - N
+    for r, u in enumerate(blocks):
+        lo, hi = u * b, min((u + 1) * b, N)
+        rows = perm[lo:hi]
+        n_u = hi - lo
+        M = token_mask_rows(rows, np.asarray(n_raster)[rows], F, H, W, gamma, keys=perm)
+        c = M.sum(dim=0).numpy()                       # per key column, tile-major
+        c = np.concatenate([c, np.zeros(pad, dtype=c.dtype)]).reshape(nb, b)
+        nonempty = (c > 0).sum(axis=1)
+        high = (3 * c > n_u).sum(axis=1)
+        if rule == "vote":
+            keep = (nonempty > 0) & (10 * high > 6 * nonempty)
+        elif rule == "union":
+            keep = nonempty > 0
+        else:
+            raise ValueError(rule)
+        keep[u] = True
+        out[r] = keep
+    return out
+
+
+def masked_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, return_lse=False):
+    """TRA attention (Sec. 3.2, Eq. 16) at block granularity: a query of block u
+    attends, with one softmax, to every key of every key block v with
+    M[u, v] = 1, and to no other key.
+
+    q, k, v: (N, d) raster order.  Returns the output rows of the queries in
+    ``blocks`` as a dict {raster row index: o_i} packed as (rows, O)."""
+    perm = np.asarray(perm, dtype=np.int64)
+    N = perm.shape[0]
+    qt, kt, vt = _t(q), _t(k), _t(v)
+    alpha = 1.0 / math.sqrt(qt.shape[1])
+    rows_out, o_out, lse_out = [], [], []
+    for r, u in enumerate(blocks):
+        rows = perm[u * b: min((u + 1) * b, N)]
+        keys = np.concatenate([perm[v * b: min((v + 1) * b, N)]
+                               for v in np.nonzero(mask_rows[r])[0]])
+        s = alpha * (qt[rows] @ kt[keys].T)
+        m = s.max(dim=1, keepdim=True).values
+        e = torch.exp(s - m)
+        z = e.sum(dim=1, keepdim=True)
+        o_out.append(((e / z) @ vt[keys]).numpy())
+        lse_out.append((m + torch.log(z))[:, 0].numpy())
+        rows_out.append(rows)
+    rows_out = np.concatenate(rows_out)
+    if return_lse:
+        return rows_out, np.concatenate(o_out), np.concatenate(lse_out)
+    return rows_out, np.concatenate(o_out)
+
+
+def retained_fraction(mask, N: int, b: int) -> float:
+    """Fraction of query-key interactions inside retained blocks,
+    sum over retained (u, v) of n_u n_v, over (heads * N^2).  mask: (..., NB, NB)."""
+    mask = np.asarray(mask, dtype=bool)
+    nb = mask.shape[-1]
+    n = np.full(nb, b, dtype=np.int64)
+    n[-1] = N - (nb - 1) * b
+    per = np.einsum("...uv,u,v->...", mask.astype(np.int64), n, n)
+    return float(np.sum(per) / (np.prod(mask.shape[:-2]) * N * N))
+
+
+# ====================================================== diagnostics
+def top_tau_support(p, tau: float) -> np.ndarray:
+    """Oracle support size K_i^tau = min{k : top-k probability mass >= tau}
+    (Sec. 3.1, Eq. 4).  A diagnostic: it needs the whole sorted row."""
+    p = p.numpy() if isinstance(p, torch.Tensor) else np.asarray(p, dtype=np.float64)
+    cs = np.cumsum(-np.sort(-p, axis=1), axis=1)
+    return (cs < tau).sum(axis=1) + 1
