@@ -1,0 +1,183 @@
+/*
+ * tra.h -- C ABI of the Token Radius Attention (TRA) hot path on MI355X (gfx950).
+ *
+ * The path (Sec. 3 of the paper) runs in four steps, one entry point each:
+ *
+ *   tra_entropy           per-query attention entropy H_i (Sec. 2.2, Eq. 2),
+ *                         accumulated inside an online-softmax pass (App. C.2,
+ *                         Alg. 2), optionally fused with the dense output O.
+ *   tra_budget_radius     entropy -> budget K_hat = ceil(tau * exp(H))
+ *                         (Sec. 3.1, Eq. 8) -> smallest boundary-aware squared
+ *                         radius reaching it (Sec. 3.2, Eqs. 13-14).
+ *   tra_build_block_mask  per-token radii -> Boolean query-block x key-block
+ *                         mask by the token vote of Alg. 1 (App. C.1), plus
+ *                         per-row lists of retained key blocks.
+ *   tra_sparse_attention  block-sparse attention over the retained blocks
+ *                         (Sec. 3.2, Eq. 16, executed at block granularity).
+ *   tra_dense_attention   dense attention (Sec. 2.1, Eq. 1), the baseline.
+ *
+ * Tensors and layout
+ * ------------------
+ * All tensor arguments are DEVICE pointers to contiguous row-major buffers on
+ * the device that was current when the plan was created.  Q, K, V and O are
+ * [batch][heads][N][head_dim] with tokens in RASTER order of the F x H x W
+ * latent grid, token i = (f*H + x)*W + y (Sec. 2.1).  Element type is bf16
+ * (TRA_BF16) or fp32 (TRA_FP32) as set in the config; pointers must be 16-byte
+ * aligned.  Per-token arrays (entropy, budget, radius_sq, lse) are
+ * [batch][heads][N], raster order.
+ *
+ * The library applies the tile-major token order of Sec. 3.3 internally: each
+ * frame is cut into tile_h x tile_w tiles (edge tiles clipped), tokens are
+ * listed frame by frame, tile by tile, row-major inside a tile, and block u is
+ * tile-major positions [u*block, min((u+1)*block, N)).  The number of blocks is
+ * NB = ceil(N / block).  Block-level arrays use row index
+ * r = (b*heads + h)*NB + u:
+ *   mask [batch][heads][NB][NB] uint8 (1 = retained),
+ *   cnt  [batch][heads][NB]     int32 (retained key blocks of row r),
+ *   cols [batch][heads][NB][NB] int32 (retained key-block ids, ascending in
+ *                               the first cnt entries, -1 after them),
+ *   order[batch*heads*NB]       int32 (a permutation of all rows r, heaviest
+ *                               first by cnt, ties by ascending r).
+ *
+ * Calls, ownership, errors
+ * ------------------------
+ * Every compute call is asynchronous on `stream` (a hipStream_t passed as
+ * void*, NULL = the null stream), checks its arguments before launching, and
+ * returns a status.  The caller owns every tensor buffer and keeps it alive
+ * until the stream has drained.  The plan owns only its small device tables
+ * and a sort workspace; it is immutable after creation, and calls that share a
+ * plan must not overlap in time on different streams when they use the
+ * sort workspace (tra_build_block_mask with a non-NULL order).  No C++
+ * exception crosses this ABI.  On failure, tra_last_error() returns a message
+ * for the calling thread.
+ */
+#ifndef TRA_H
+#define TRA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Squared radius of the full-support candidate radius of Sec. 3.2 (keeps
+ * every key of every frame). */
+#define TRA_RADIUS_FULL 2147483647
+
+typedef enum {
+  TRA_OK = 0,
+  TRA_ERR_INVALID_ARG = 1, /* null pointer, bad shape or misaligned buffer   */
+  TRA_ERR_UNSUPPORTED = 2, /* head_dim / block / dtype / device not handled   */
+  TRA_ERR_DEVICE = 3,      /* a HIP runtime call or kernel launch failed      */
+  TRA_ERR_ALLOC = 4        /* plan table allocation failed                    */
+} tra_status;
+
+typedef enum { TRA_BF16 = 0, TRA_FP32 = 1 } tra_dtype;
+
+/* Block retention rule.  VOTE is Alg. 1: with c_j the number of valid queries
+ * of the query block whose radius covers key j, C = {j : c_j > 0} and
+ * C_hi = {j : 3 c_j > n_u} (n_u = valid queries of the block, b/3 for a full
+ * block), keep iff |C| > 0 and 10 |C_hi| > 6 |C|.  UNION keeps iff |C| > 0.
+ * Under both rules the diagonal block (u, u) is always kept. */
+typedef enum { TRA_MASK_VOTE = 0, TRA_MASK_UNION = 1 } tra_mask_rule;
+
+typedef struct tra_config {
+  int32_t batch;     /* >= 1                                                  */
+  int32_t heads;     /* >= 1                                                  */
+  int32_t frames;    /* F >= 1 (at most 64)                                   */
+  int32_t height;    /* H >= 1 (latent rows, at most 1023)                    */
+  int32_t width;     /* W >= 1 (latent columns, at most 1023)                 */
+  int32_t head_dim;  /* d: 64 or 128                                          */
+  int32_t block;     /* b: 64 or 128 (bf16 needs 128)                         */
+  int32_t tile_h;    /* tile rows >= 1 (typ. 8)                               */
+  int32_t tile_w;    /* tile columns >= 1 (typ. 8 for b=64, 16 for b=128)     */
+  int32_t dtype;     /* tra_dtype                                             */
+  int32_t rule;      /* tra_mask_rule                                         */
+  int32_t reserved;  /* must be 0                                             */
+  double tau;        /* target attention mass, 0 < tau < 1 (paper: 0.9)      */
+  double gamma;      /* temporal decay rate of phi(delta) = exp(-gamma delta),
+                        gamma >= 0 (Eq. 10; 0.6 Wan, 0.95 HunyuanVideo)       */
+} tra_config;
+
+typedef struct tra_plan_s* tra_plan;
+
+/* Validates cfg, builds the shape tables on the host in fp64/integer
+ * arithmetic (tile-major permutation, squared-radius thresholds
+ * thr[n][delta] = floor(n * exp(-2 gamma delta)) for n in [0, n_cap],
+ * n_cap = (H-1)^2 + (W-1)^2, per-block bounding boxes) and copies them to
+ * the current device.  *out receives the plan, or NULL on failure. */
+tra_status tra_plan_create(const tra_config* cfg, tra_plan* out);
+
+/* Frees the plan's device tables.  NULL is accepted. */
+tra_status tra_plan_destroy(tra_plan plan);
+
+/* N = F*H*W, NB = ceil(N / block), n_cap as above.  Any output may be NULL. */
+tra_status tra_plan_dims(tra_plan plan, int32_t* n_tokens, int32_t* n_blocks,
+                         int32_t* n_cap);
+
+/* Host-only (no device needed): the plan's tables for cfg, for inspection.
+ * perm[N]: raster index of the token at tile-major position p.
+ * thr[(n_cap+1) * F]: thr[n*F + delta].
+ * blocks[NB * 8]: per block {f_min, f_max, x_min, x_max, y_min, y_max,
+ *                 n_valid, 0} over its valid tokens.
+ * Any array pointer may be NULL; *n_cap_out (may be NULL) gets n_cap. */
+tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
+                                int32_t* blocks, int32_t* n_cap_out);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* tra_last_error(void);
+
+/* Library version string. */
+const char* tra_version(void);
+
+/* Attention entropy H_i = -sum_j p_ij log p_ij in nats over all N keys
+ * (Eq. 2), computed with the online-softmax identity
+ * H = log Z - sum_j p_ij s_ij of App. C.2 (Alg. 2).
+ * q, k: inputs.  v, o: both NULL (entropy only), or both non-NULL, in which
+ * case o also receives dense attention softmax(q k^T / sqrt(d)) v, bitwise equal
+ * to tra_dense_attention's output (the fused warm-up step of Alg. 2).
+ * entropy: fp32 [batch][heads][N] output. */
+tra_status tra_entropy(tra_plan plan, const void* q, const void* k, const void* v,
+                       void* o, float* entropy, void* stream);
+
+/* Entropy -> budget -> squared radius, per token (Sec. 3.1-3.2; App. C.1,
+ * Eq. implementation-budget-radius).
+ * K_hat = min(max(ceil(tau * exp((double)H)), 1), N) evaluated in fp64.
+ * radius_sq = the smallest n in [0, n_cap] whose boundary-aware count
+ * C(n) = sum_t #{(x', y') : (x-x')^2 + (y-y')^2 <= thr[n][|t - f|]} (Eq. 13)
+ * reaches K_hat (Eq. 14), else TRA_RADIUS_FULL.  Counts are exact integers.
+ * entropy: fp32 input; budget: int32 output or NULL; radius_sq: int32 output. */
+tra_status tra_budget_radius(tra_plan plan, const float* entropy, int32_t* budget,
+                             int32_t* radius_sq, void* stream);
+
+/* Alg. 1 block mask from per-token squared radii (raster order).  A query i
+ * covers key j iff (x_i-x_j)^2 + (y_i-y_j)^2 <= thr[n_i][|f_i - f_j|]
+ * (Eq. 15); radius values outside [0, n_cap] other than TRA_RADIUS_FULL are
+ * clamped (negative -> 0, larger -> FULL).  The rule comes from the plan.
+ * mask: uint8 output or NULL; cnt, cols: int32 outputs; order: int32 output or
+ * NULL (uses the plan's sort workspace). */
+tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t* mask,
+                                int32_t* cnt, int32_t* cols, int32_t* order,
+                                void* stream);
+
+/* Block-sparse attention: a query of block u takes one softmax over every key
+ * of the key blocks cols[r][0..cnt[r]) (r its row) and attends to no other key
+ * (Eq. 16 at block granularity).  Rows are processed in `order` when it is
+ * non-NULL (entries outside [0, rows) are skipped), else in row order.
+ * cnt values are clamped to [0, NB]; column ids outside [0, NB) are skipped.
+ * o: output; lse: fp32 natural-log log-sum-exp of the scaled scores over the
+ * retained keys, or NULL.  A row with cnt = 0 gets o = 0, lse = -inf. */
+tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
+                                const void* v, const int32_t* cnt, const int32_t* cols,
+                                const int32_t* order, void* o, float* lse, void* stream);
+
+/* Dense attention o_i = sum_j softmax_j(q_i k_j / sqrt(d)) v_j (Eq. 1), the
+ * baseline the sparse call is measured against.  lse as above, or NULL. */
+tra_status tra_dense_attention(tra_plan plan, const void* q, const void* k,
+                               const void* v, void* o, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRA_H */

@@ -1,0 +1,296 @@
+"""Token Radius Attention hot path on MI355X (gfx950): Python binding.
+
+Thin ctypes binding of libtra.so (C ABI declared in include/tra.h).  It only
+marshals arguments: every step of the path runs in the library's HIP kernels.
+torch is used for device memory and streams.  The functions keep the C names:
+
+    tra_plan_create / tra_plan_destroy / tra_plan_dims / tra_plan_host_tables
+    tra_entropy / tra_budget_radius / tra_build_block_mask
+    tra_sparse_attention / tra_dense_attention
+
+There is no fallback: if libtra.so is missing or fails to load, every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+__all__ = [
+    "LIB_PATH", "TRA_RADIUS_FULL", "TraError", "Config", "Plan", "lib", "library_loaded",
+    "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
+    "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
+    "tra_sparse_attention", "tra_dense_attention", "tra_version", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtra.so")
+TRA_RADIUS_FULL = 2 ** 31 - 1
+TRA_BF16, TRA_FP32 = 0, 1
+TRA_MASK_VOTE, TRA_MASK_UNION = 0, 1
+
+EXPORTED_SYMBOLS = (
+    "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
+    "tra_last_error", "tra_version", "tra_entropy", "tra_budget_radius",
+    "tra_build_block_mask", "tra_sparse_attention", "tra_dense_attention",
+)
+
+_STATUS = {0: "TRA_OK", 1: "TRA_ERR_INVALID_ARG", 2: "TRA_ERR_UNSUPPORTED",
+           3: "TRA_ERR_DEVICE", 4: "TRA_ERR_ALLOC"}
+
+
+class TraError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "batch", "heads", "frames", "height", "width", "head_dim", "block",
+        "tile_h", "tile_w", "dtype", "rule", "reserved")] + [
+        ("tau", ctypes.c_double), ("gamma", ctypes.c_double)]
+
+
+@dataclass(frozen=True)
+class Config:
+    """Shape and policy of one attention call (mirrors struct tra_config)."""
+    batch: int
+    heads: int
+    frames: int
+    height: int
+    width: int
+    head_dim: int
+    block: int = 128
+    tile_h: int = 8
+    tile_w: int = 16
+    dtype: str = "bf16"       # "bf16" or "fp32"
+    rule: str = "vote"        # "vote" (Alg. 1) or "union"
+    tau: float = 0.9
+    gamma: float = 0.6
+
+    @property
+    def n_tokens(self) -> int:
+        return self.frames * self.height * self.width
+
+    @property
+    def n_blocks(self) -> int:
+        return -(-self.n_tokens // self.block)
+
+    def to_c(self) -> _Config:
+        return _Config(self.batch, self.heads, self.frames, self.height, self.width,
+                       self.head_dim, self.block, self.tile_h, self.tile_w,
+                       TRA_BF16 if self.dtype == "bf16" else TRA_FP32 if self.dtype == "fp32" else 99,
+                       TRA_MASK_VOTE if self.rule == "vote" else TRA_MASK_UNION if self.rule == "union" else 99,
+                       0, self.tau, self.gamma)
+
+    @classmethod
+    def from_workload(cls, w, **kw) -> "Config":
+        base = dict(batch=w.batch, heads=w.heads, frames=w.frames, height=w.height,
+                    width=w.width, head_dim=w.head_dim, block=w.block, tile_h=w.tile_h,
+                    tile_w=w.tile_w, dtype=w.dtype, tau=w.tau, gamma=w.gamma)
+        base.update(kw)
+        return cls(**base)
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libtra.so (once).  Raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run python -m paper_2608_02504_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, V = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
+    cfgp = ctypes.POINTER(_Config)
+    L.tra_plan_create.argtypes = [cfgp, ctypes.POINTER(P)]
+    L.tra_plan_destroy.argtypes = [P]
+    L.tra_plan_dims.argtypes = [P, P, P, P]
+    L.tra_plan_host_tables.argtypes = [cfgp, P, P, P, P]
+    L.tra_last_error.restype = ctypes.c_char_p
+    L.tra_version.restype = ctypes.c_char_p
+    L.tra_entropy.argtypes = [P, V, V, V, V, V, V]
+    L.tra_budget_radius.argtypes = [P, V, V, V, V]
+    L.tra_build_block_mask.argtypes = [P, V, V, V, V, V, V]
+    L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V]
+    L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V]
+    for name in ("tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
+                 "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
+                 "tra_sparse_attention", "tra_dense_attention"):
+        getattr(L, name).restype = I
+    _lib = L
+    return L
+
+
+def library_loaded() -> bool:
+    return _lib is not None
+
+
+def _check(status: int):
+    if status != 0:
+        raise TraError(status, lib().tra_last_error().decode())
+
+
+def tra_version() -> str:
+    return lib().tra_version().decode()
+
+
+# ------------------------------------------------------------------ plans
+class Plan:
+    """Owns a tra_plan (device tables for one shape)."""
+
+    def __init__(self, cfg: Config):
+        self.cfg = cfg
+        self._c = cfg.to_c()
+        h = ctypes.c_void_p()
+        _check(lib().tra_plan_create(ctypes.byref(self._c), ctypes.byref(h)))
+        self.handle = h
+        n, nb, cap = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().tra_plan_dims(h, ctypes.byref(n), ctypes.byref(nb), ctypes.byref(cap)))
+        self.n_tokens, self.n_blocks, self.n_cap = n.value, nb.value, cap.value
+
+    @property
+    def rows(self) -> int:
+        return self.cfg.batch * self.cfg.heads * self.n_blocks
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().tra_plan_destroy(self.handle)
+            self.handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def tra_plan_create(cfg: Config) -> Plan:
+    return Plan(cfg)
+
+
+def tra_plan_destroy(plan: Plan):
+    plan.close()
+
+
+def tra_plan_dims(plan: Plan):
+    return plan.n_tokens, plan.n_blocks, plan.n_cap
+
+
+def tra_plan_host_tables(cfg: Config):
+    """Host-only tables of cfg: (perm[N], thr[(n_cap+1), F], blocks[NB, 8], n_cap)."""
+    c = cfg.to_c()
+    cap = ctypes.c_int32()
+    _check(lib().tra_plan_host_tables(ctypes.byref(c), None, None, None, ctypes.byref(cap)))
+    perm = np.empty(cfg.n_tokens, dtype=np.int32)
+    thr = np.empty((cap.value + 1, cfg.frames), dtype=np.int32)
+    blocks = np.empty((cfg.n_blocks, 8), dtype=np.int32)
+    _check(lib().tra_plan_host_tables(ctypes.byref(c), perm.ctypes.data, thr.ctypes.data,
+                                      blocks.ctypes.data, ctypes.byref(cap)))
+    return perm, thr, blocks, cap.value
+
+
+# ------------------------------------------------------------------ marshalling
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _want(t, shape, dtype, name):
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{name}: expected {tuple(shape)} {dtype}, got {tuple(t.shape)} {t.dtype}")
+
+
+def _qkv_dtype(plan: Plan):
+    import torch
+    return torch.bfloat16 if plan.cfg.dtype == "bf16" else torch.float32
+
+
+def _shapes(plan: Plan):
+    c = plan.cfg
+    return ((c.batch, c.heads, plan.n_tokens, c.head_dim), (c.batch, c.heads, plan.n_tokens),
+            (c.batch, c.heads, plan.n_blocks), (c.batch, c.heads, plan.n_blocks, plan.n_blocks))
+
+
+def tra_entropy(plan: Plan, q, k, v, o, entropy, stream=None):
+    import torch
+    tok, per, _, _ = _shapes(plan)
+    dt = _qkv_dtype(plan)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _want(t, tok, dt, n)
+    _want(entropy, per, torch.float32, "entropy")
+    _check(lib().tra_entropy(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(entropy),
+                             _stream(stream)))
+
+
+def tra_budget_radius(plan: Plan, entropy, budget, radius_sq, stream=None):
+    import torch
+    _, per, _, _ = _shapes(plan)
+    _want(entropy, per, torch.float32, "entropy")
+    _want(budget, per, torch.int32, "budget")
+    _want(radius_sq, per, torch.int32, "radius_sq")
+    _check(lib().tra_budget_radius(plan.handle, _ptr(entropy), _ptr(budget), _ptr(radius_sq),
+                                   _stream(stream)))
+
+
+def tra_build_block_mask(plan: Plan, radius_sq, mask, cnt, cols, order=None, stream=None):
+    import torch
+    _, per, rowsh, sq = _shapes(plan)
+    _want(radius_sq, per, torch.int32, "radius_sq")
+    _want(mask, sq, torch.uint8, "mask")
+    _want(cnt, rowsh, torch.int32, "cnt")
+    _want(cols, sq, torch.int32, "cols")
+    _want(order, (plan.rows,), torch.int32, "order")
+    _check(lib().tra_build_block_mask(plan.handle, _ptr(radius_sq), _ptr(mask), _ptr(cnt),
+                                      _ptr(cols), _ptr(order), _stream(stream)))
+
+
+def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, stream=None):
+    import torch
+    tok, per, rowsh, sq = _shapes(plan)
+    dt = _qkv_dtype(plan)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _want(t, tok, dt, n)
+    _want(cnt, rowsh, torch.int32, "cnt")
+    _want(cols, sq, torch.int32, "cols")
+    _want(order, (plan.rows,), torch.int32, "order")
+    _want(lse, per, torch.float32, "lse")
+    _check(lib().tra_sparse_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(cnt),
+                                      _ptr(cols), _ptr(order), _ptr(o), _ptr(lse),
+                                      _stream(stream)))
+
+
+def tra_dense_attention(plan: Plan, q, k, v, o, lse=None, stream=None):
+    import torch
+    tok, per, _, _ = _shapes(plan)
+    dt = _qkv_dtype(plan)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _want(t, tok, dt, n)
+    _want(lse, per, torch.float32, "lse")
+    _check(lib().tra_dense_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                     _stream(stream)))

@@ -1,0 +1,249 @@
+// C ABI entry points of the TRA library: argument checks, plan lifetime,
+// dispatch to the kernel launchers.  No exception leaves this file.
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "tra_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tra_status fail(tra_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+tra_status ok() {
+  g_last_error.clear();
+  return TRA_OK;
+}
+
+tra_status hip_fail(hipError_t e, const char* what) {
+  return fail(TRA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// The plan's device must be current: kernels index the plan's tables.
+tra_status check_plan(tra_plan p) {
+  if (!p) return fail(TRA_ERR_INVALID_ARG, "plan is NULL");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != p->device)
+    return fail(TRA_ERR_INVALID_ARG, "current device differs from the plan's device");
+  return TRA_OK;
+}
+
+tra_status check_tensor(const void* ptr, const char* name, bool nullable = false) {
+  if (!ptr) {
+    if (nullable) return TRA_OK;
+    return fail(TRA_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  }
+  if (!aligned16(ptr)) return fail(TRA_ERR_INVALID_ARG, std::string(name) + " is not 16-byte aligned");
+  return TRA_OK;
+}
+
+tra_status check_aligned4(const void* ptr, const char* name, bool nullable) {
+  if (!ptr) {
+    if (nullable) return TRA_OK;
+    return fail(TRA_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  }
+  if (((uintptr_t)ptr & 3u) != 0) return fail(TRA_ERR_INVALID_ARG, std::string(name) + " is not 4-byte aligned");
+  return TRA_OK;
+}
+
+#define TRA_TRY(expr)                   \
+  do {                                  \
+    tra_status _s = (expr);             \
+    if (_s != TRA_OK) return _s;        \
+  } while (0)
+
+tra_status launch_result(hipError_t e, const char* what) {
+  if (e != hipSuccess) return hip_fail(e, what);
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tra_last_error(void) { return g_last_error.c_str(); }
+
+const char* tra_version(void) { return "tra-mi355x 0.1 (gfx950)"; }
+
+tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
+                                int32_t* blocks, int32_t* n_cap_out) {
+  try {
+    std::string why;
+    tra_status s = tra::validate_config(cfg, &why);
+    if (s != TRA_OK) return fail(s, why);
+    tra::HostTables t;
+    tra::build_host_tables(*cfg, &t, perm != nullptr, thr != nullptr, blocks != nullptr);
+    if (perm) std::memcpy(perm, t.perm.data(), t.perm.size() * sizeof(int32_t));
+    if (thr) std::memcpy(thr, t.thr.data(), t.thr.size() * sizeof(int32_t));
+    if (blocks) std::memcpy(blocks, t.blocks.data(), t.blocks.size() * sizeof(int32_t));
+    if (n_cap_out) *n_cap_out = t.n_cap;
+    return ok();
+  } catch (const std::bad_alloc&) {
+    return fail(TRA_ERR_ALLOC, "host allocation failed");
+  } catch (...) {
+    return fail(TRA_ERR_INVALID_ARG, "unexpected error building host tables");
+  }
+}
+
+tra_status tra_plan_destroy(tra_plan p) {
+  if (!p) return ok();
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(p->device);
+  (void)hipFree(p->d_perm);
+  (void)hipFree(p->d_coord);
+  (void)hipFree(p->d_thr);
+  (void)hipFree(p->d_blocks);
+  (void)hipFree(p->d_sort_ws);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  delete p;
+  return ok();
+}
+
+tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
+  if (!out) return fail(TRA_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  try {
+    std::string why;
+    tra_status s = tra::validate_config(cfg, &why);
+    if (s != TRA_OK) return fail(s, why);
+
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+      return fail(TRA_ERR_UNSUPPORTED, std::string("device is ") + prop.gcnArchName + ", not gfx950");
+
+    tra::HostTables t;
+    tra::build_host_tables(*cfg, &t, true, true, true);
+
+    tra_plan p = new tra_plan_s();
+    p->cfg = *cfg;
+    p->device = dev;
+    p->N = t.N;
+    p->NB = t.NB;
+    p->n_cap = t.n_cap;
+    p->rows = cfg->batch * cfg->heads * t.NB;
+    p->sort_chunks = (p->rows + tra::kSortChunk - 1) / tra::kSortChunk;
+    // chunk histograms over keys 0..NB, plus one total slot
+    p->sort_ws_elems = (int64_t)(t.NB + 1) * p->sort_chunks + 1;
+
+    auto upload = [&](int32_t** dst, const std::vector<int32_t>& src) -> hipError_t {
+      hipError_t err = hipMalloc((void**)dst, src.size() * sizeof(int32_t));
+      if (err != hipSuccess) return err;
+      return hipMemcpy(*dst, src.data(), src.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    };
+    if ((e = upload(&p->d_perm, t.perm)) != hipSuccess ||
+        (e = upload(&p->d_coord, t.coord)) != hipSuccess ||
+        (e = upload(&p->d_thr, t.thr)) != hipSuccess ||
+        (e = upload(&p->d_blocks, t.blocks)) != hipSuccess ||
+        (e = hipMalloc((void**)&p->d_sort_ws, p->sort_ws_elems * sizeof(int32_t))) != hipSuccess) {
+      tra_plan_destroy(p);
+      return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
+    }
+    *out = p;
+    return ok();
+  } catch (const std::bad_alloc&) {
+    return fail(TRA_ERR_ALLOC, "host allocation failed");
+  } catch (...) {
+    return fail(TRA_ERR_INVALID_ARG, "unexpected error creating plan");
+  }
+}
+
+tra_status tra_plan_dims(tra_plan p, int32_t* n_tokens, int32_t* n_blocks, int32_t* n_cap) {
+  if (!p) return fail(TRA_ERR_INVALID_ARG, "plan is NULL");
+  if (n_tokens) *n_tokens = p->N;
+  if (n_blocks) *n_blocks = p->NB;
+  if (n_cap) *n_cap = p->n_cap;
+  return ok();
+}
+
+static tra_status run_attention(tra_plan p, const tra::AttnArgs& a, void* stream, const char* what) {
+  hipError_t e = p->cfg.dtype == TRA_BF16
+                     ? tra::launch_attention_bf16(*p, a, (hipStream_t)stream)
+                     : tra::launch_attention_f32(*p, a, (hipStream_t)stream);
+  return launch_result(e, what);
+}
+
+tra_status tra_entropy(tra_plan p, const void* q, const void* k, const void* v, void* o,
+                       float* entropy, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_tensor(q, "q"));
+  TRA_TRY(check_tensor(k, "k"));
+  TRA_TRY(check_tensor(v, "v", true));
+  TRA_TRY(check_tensor(o, "o", true));
+  TRA_TRY(check_aligned4(entropy, "entropy", false));
+  if ((v == nullptr) != (o == nullptr))
+    return fail(TRA_ERR_INVALID_ARG, "v and o must be both NULL or both non-NULL");
+  tra::AttnArgs a{q, k, v, o, nullptr, entropy, nullptr, nullptr, nullptr, false};
+  return run_attention(p, a, stream, "tra_entropy launch");
+}
+
+tra_status tra_budget_radius(tra_plan p, const float* entropy, int32_t* budget,
+                             int32_t* radius_sq, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_aligned4(entropy, "entropy", false));
+  TRA_TRY(check_aligned4(budget, "budget", true));
+  TRA_TRY(check_aligned4(radius_sq, "radius_sq", false));
+  return launch_result(tra::launch_budget_radius(*p, entropy, budget, radius_sq, (hipStream_t)stream),
+                       "tra_budget_radius launch");
+}
+
+tra_status tra_build_block_mask(tra_plan p, const int32_t* radius_sq, uint8_t* mask,
+                                int32_t* cnt, int32_t* cols, int32_t* order, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_aligned4(radius_sq, "radius_sq", false));
+  TRA_TRY(check_aligned4(cnt, "cnt", false));
+  TRA_TRY(check_aligned4(cols, "cols", false));
+  TRA_TRY(check_aligned4(order, "order", true));
+  hipError_t e = tra::launch_block_mask(*p, radius_sq, mask, cnt, cols, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask launch");
+  if (order) {
+    e = tra::launch_row_order(*p, cnt, order, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask order launch");
+  }
+  return ok();
+}
+
+tra_status tra_sparse_attention(tra_plan p, const void* q, const void* k, const void* v,
+                                const int32_t* cnt, const int32_t* cols, const int32_t* order,
+                                void* o, float* lse, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_tensor(q, "q"));
+  TRA_TRY(check_tensor(k, "k"));
+  TRA_TRY(check_tensor(v, "v"));
+  TRA_TRY(check_tensor(o, "o"));
+  TRA_TRY(check_aligned4(cnt, "cnt", false));
+  TRA_TRY(check_aligned4(cols, "cols", false));
+  TRA_TRY(check_aligned4(order, "order", true));
+  TRA_TRY(check_aligned4(lse, "lse", true));
+  tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true};
+  return run_attention(p, a, stream, "tra_sparse_attention launch");
+}
+
+tra_status tra_dense_attention(tra_plan p, const void* q, const void* k, const void* v,
+                               void* o, float* lse, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_tensor(q, "q"));
+  TRA_TRY(check_tensor(k, "k"));
+  TRA_TRY(check_tensor(v, "v"));
+  TRA_TRY(check_tensor(o, "o"));
+  TRA_TRY(check_aligned4(lse, "lse", true));
+  tra::AttnArgs a{q, k, v, o, lse, nullptr, nullptr, nullptr, nullptr, false};
+  return run_attention(p, a, stream, "tra_dense_attention launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,264 @@
+// Token-radius block mask (App. C.1, Alg. 1) and the heaviest-first row order.
+//
+// One workgroup per query-block row (batch, head, u); its four waves walk the
+// key blocks v.  For a key column j of block v, c_j counts the valid queries
+// i of u whose radius covers j (Eq. 15):
+//     (x_i - x_j)^2 + (y_i - y_j)^2 <= thr[n_i][|f_i - f_j|].
+// Alg. 1 evaluates every (i, j) pair.  Here each query is first classified
+// against the bounding box of v (App. C.1 uses such boxes to reject whole
+// block pairs): "none" if even the nearest box point in the most favourable
+// frame is outside its disk, "all" if the farthest box point in the least
+// favourable frame is inside.  Only "partial" queries are tested key by key,
+// so the counts -- and the mask -- are exactly Alg. 1's; the boxes only skip
+// work whose outcome is already known.  Everything is integer arithmetic.
+#include <climits>
+
+#include "tra_internal.h"
+
+namespace tra {
+namespace {
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
+
+template <int B, int RULE>
+__global__ __launch_bounds__(256) void block_mask_kernel(
+    const int32_t* __restrict__ radius_sq, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ coord, const int32_t* __restrict__ thr,
+    const int32_t* __restrict__ binfo, uint8_t* __restrict__ mask, int32_t* __restrict__ cnt,
+    int32_t* __restrict__ cols, int N, int NB, int F, int n_cap) {
+  constexpr int QPL = B / 64;  // queries (and keys) per lane
+  __shared__ int32_t s_T[B * kMaxFrames];  // s_T[q*F + delta]: squared-distance threshold of query q
+  __shared__ int32_t s_c[B];               // packed coordinate of query q
+  __shared__ uint8_t s_keep[kMaxBlocks];
+
+  const int row = blockIdx.x;
+  const int bh = row / NB, u = row - bh * NB;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int q0 = u * B;
+  const int n_u = min(B, N - q0);
+
+  for (int qi = t; qi < B; qi += blockDim.x) {
+    if (qi < n_u) {
+      const int pos = q0 + qi;
+      int n = radius_sq[(size_t)bh * N + perm[pos]];
+      const bool full = n > n_cap;  // TRA_RADIUS_FULL and anything above the cap
+      n = max(n, 0);
+      s_c[qi] = coord[pos];
+      for (int d = 0; d < F; ++d) s_T[qi * F + d] = full ? INT_MAX : thr[(size_t)n * F + d];
+    } else {
+      s_c[qi] = 0;
+      for (int d = 0; d < F; ++d) s_T[qi * F + d] = -1;  // covers nothing: D >= 0 > -1
+    }
+  }
+  __syncthreads();
+
+  // This lane's queries, fixed for the whole row.
+  int qx[QPL], qy[QPL], qf[QPL];
+  bool qvalid[QPL];
+#pragma unroll
+  for (int s = 0; s < QPL; ++s) {
+    const int qi = lane + 64 * s;
+    const int c = s_c[qi];
+    qx[s] = coord_x(c); qy[s] = coord_y(c); qf[s] = coord_f(c);
+    qvalid[s] = qi < n_u;
+  }
+
+  for (int v = wave; v < NB; v += 4) {
+    bool keep;
+    if (v == u) {
+      keep = true;  // every query keeps its own key, so the diagonal block is never empty
+    } else {
+      const int32_t* bi = binfo + (size_t)v * kBlockInfo;
+      const int fmin = bi[0], fmax = bi[1], xmin = bi[2], xmax = bi[3];
+      const int ymin = bi[4], ymax = bi[5], n_v = bi[6];
+      uint64_t all_m[QPL], part_m[QPL];
+      int n_all = 0;
+      bool any_part = false;
+#pragma unroll
+      for (int s = 0; s < QPL; ++s) {
+        const int qi = lane + 64 * s;
+        const int dxn = max(0, max(xmin - qx[s], qx[s] - xmax));
+        const int dyn = max(0, max(ymin - qy[s], qy[s] - ymax));
+        const int dxf = max(qx[s] - xmin, xmax - qx[s]);
+        const int dyf = max(qy[s] - ymin, ymax - qy[s]);
+        const int dmin = qf[s] < fmin ? fmin - qf[s] : (qf[s] > fmax ? qf[s] - fmax : 0);
+        const int dmax = max(qf[s] - fmin, fmax - qf[s]);
+        const int t_hi = s_T[qi * F + dmin];  // thresholds are non-increasing in delta
+        const int t_lo = s_T[qi * F + dmax];
+        const bool none = !qvalid[s] || dxn * dxn + dyn * dyn > t_hi;
+        const bool all = qvalid[s] && dxf * dxf + dyf * dyf <= t_lo;
+        all_m[s] = ballot(all);
+        part_m[s] = ballot(!none && !all);
+        n_all += popc(all_m[s]);
+        any_part |= part_m[s] != 0;
+      }
+      if (RULE == TRA_MASK_VOTE && 3 * n_all > n_u) {
+        keep = true;   // every column already has c_j >= n_all > n_u / 3
+      } else if (RULE == TRA_MASK_UNION && n_all > 0) {
+        keep = true;
+      } else if (!any_part) {
+        // every column has c_j = n_all; under the vote, 3 n_all <= n_u here
+        keep = false;
+      } else {
+        int kx[QPL], ky[QPL], kf[QPL], c[QPL];
+        bool kvalid[QPL];
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+          const int j = lane + 64 * s;
+          kvalid[s] = j < n_v;
+          const int cc = kvalid[s] ? coord[(size_t)v * B + j] : 0;
+          kx[s] = coord_x(cc); ky[s] = coord_y(cc); kf[s] = coord_f(cc);
+          c[s] = n_all;
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < QPL; ++s2) {
+          uint64_t m = part_m[s2];
+          while (m) {
+            const int qi = __ffsll((unsigned long long)m) - 1 + 64 * s2;
+            m &= m - 1;
+            const int pc = s_c[qi];
+            const int px = coord_x(pc), py = coord_y(pc), pf = coord_f(pc);
+            const int32_t* Tp = s_T + qi * F;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+              const int dx = px - kx[s], dy = py - ky[s];
+              const int dl = abs(pf - kf[s]);
+              c[s] += (dx * dx + dy * dy <= Tp[dl]) ? 1 : 0;
+            }
+          }
+        }
+        int nonempty = 0, high = 0;
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+          nonempty += popc(ballot(kvalid[s] && c[s] > 0));
+          high += popc(ballot(kvalid[s] && 3 * c[s] > n_u));
+        }
+        keep = RULE == TRA_MASK_VOTE ? (nonempty > 0 && 10 * high > 6 * nonempty) : nonempty > 0;
+      }
+    }
+    if (lane == 0) {
+      s_keep[v] = keep ? 1 : 0;
+      if (mask) mask[(size_t)row * NB + v] = keep ? 1 : 0;
+    }
+  }
+  __syncthreads();
+
+  // Compact the retained key blocks of this row in ascending order.
+  if (wave == 0) {
+    int base = 0;
+    for (int v0 = 0; v0 < NB; v0 += 64) {
+      const int v = v0 + lane;
+      const bool k = v < NB && s_keep[v];
+      const uint64_t bm = ballot(k);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bm >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bm, 0u));
+      if (k) cols[(size_t)row * NB + base + rank] = v;
+      base += popc(bm);
+    }
+    for (int i = base + lane; i < NB; i += 64) cols[(size_t)row * NB + i] = -1;
+    if (lane == 0) cnt[row] = base;
+  }
+}
+
+// ------------------------------------------------ heaviest-first row order
+// Stable counting sort of rows by key NB - cnt (so larger cnt first, ties by
+// row index): per-chunk histograms, one exclusive scan in (key, chunk) order,
+// then a scatter that ranks equal keys inside a chunk by row index.
+
+__global__ __launch_bounds__(kSortChunk) void order_hist_kernel(const int32_t* __restrict__ cnt,
+                                                                int32_t* __restrict__ ws, int rows,
+                                                                int NB, int chunks) {
+  __shared__ int32_t h[kMaxBlocks + 1];
+  for (int i = threadIdx.x; i <= NB; i += blockDim.x) h[i] = 0;
+  __syncthreads();
+  const int r = blockIdx.x * kSortChunk + threadIdx.x;
+  if (r < rows) atomicAdd(&h[NB - min(max(cnt[r], 0), NB)], 1);
+  __syncthreads();
+  for (int k = threadIdx.x; k <= NB; k += blockDim.x) ws[(size_t)k * chunks + blockIdx.x] = h[k];
+}
+
+__global__ __launch_bounds__(1024) void order_scan_kernel(int32_t* __restrict__ ws, int L) {
+  __shared__ int32_t part[1024];
+  const int t = threadIdx.x;
+  const int per = (L + 1023) / 1024;
+  const int lo = min(L, t * per), hi = min(L, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += ws[i];
+  part[t] = s;
+  __syncthreads();
+  if (t == 0) {
+    int run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int x = part[i];
+      part[i] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  int run = part[t];
+  for (int i = lo; i < hi; ++i) {
+    const int x = ws[i];
+    ws[i] = run;
+    run += x;
+  }
+}
+
+__global__ __launch_bounds__(kSortChunk) void order_scatter_kernel(const int32_t* __restrict__ cnt,
+                                                                   const int32_t* __restrict__ ws,
+                                                                   int32_t* __restrict__ order,
+                                                                   int rows, int NB, int chunks) {
+  __shared__ int32_t keys[kSortChunk];
+  const int t = threadIdx.x;
+  const int r = blockIdx.x * kSortChunk + t;
+  const int key = r < rows ? NB - min(max(cnt[r], 0), NB) : -1;
+  keys[t] = key;
+  __syncthreads();
+  if (r < rows) {
+    int rank = 0;
+    for (int s = 0; s < t; ++s) rank += keys[s] == key;
+    order[ws[(size_t)key * chunks + blockIdx.x] + rank] = r;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask,
+                             int32_t* cnt, int32_t* cols, hipStream_t s) {
+  const dim3 grid(p.rows), block(256);
+  const int F = p.cfg.frames;
+  const bool vote = p.cfg.rule == TRA_MASK_VOTE;
+  if (p.cfg.block == 128) {
+    if (vote)
+      hipLaunchKernelGGL((block_mask_kernel<128, TRA_MASK_VOTE>), grid, block, 0, s, radius_sq, p.d_perm,
+                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
+    else
+      hipLaunchKernelGGL((block_mask_kernel<128, TRA_MASK_UNION>), grid, block, 0, s, radius_sq, p.d_perm,
+                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
+  } else {
+    if (vote)
+      hipLaunchKernelGGL((block_mask_kernel<64, TRA_MASK_VOTE>), grid, block, 0, s, radius_sq, p.d_perm,
+                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
+    else
+      hipLaunchKernelGGL((block_mask_kernel<64, TRA_MASK_UNION>), grid, block, 0, s, radius_sq, p.d_perm,
+                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_row_order(const tra_plan_s& p, const int32_t* cnt, int32_t* order, hipStream_t s) {
+  const int chunks = p.sort_chunks;
+  hipLaunchKernelGGL(order_hist_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, p.d_sort_ws, p.rows,
+                     p.NB, chunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, s, p.d_sort_ws,
+                     (int)((int64_t)(p.NB + 1) * chunks));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(order_scatter_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, p.d_sort_ws, order,
+                     p.rows, p.NB, chunks);
+  return hipGetLastError();
+}
+
+}  // namespace tra

@@ -1,0 +1,104 @@
+// Shape tables of a TRA plan, built on the host in integer / fp64 arithmetic.
+//
+//  * tile-major order of Sec. 3.3 ("Flash Radius Mask Kernel") and App. C.1
+//    ("Kernel execution"): frames in order, each frame cut into
+//    tile_h x tile_w tiles (edge tiles clipped), tiles in row-major tile
+//    order, tokens row-major inside a tile;
+//  * squared-radius thresholds: for squared base radius n (r = sqrt n) and
+//    temporal distance delta, the test d_s <= r * phi(delta) of Eq. 15 with
+//    phi(delta) = exp(-gamma delta) (Eq. 10) holds for an integer squared
+//    distance D iff D <= floor(n * exp(-2 gamma delta));
+//  * per-block bounding boxes used to skip block pairs (App. C.1, "Kernel
+//    execution": a bounding-box test rejects pairs with no valid
+//    interaction).
+#include <algorithm>
+#include <cmath>
+
+#include "tra_internal.h"
+
+namespace tra {
+
+tra_status validate_config(const tra_config* cfg, std::string* why) {
+  if (!cfg) { *why = "config is NULL"; return TRA_ERR_INVALID_ARG; }
+  const tra_config& c = *cfg;
+  if (c.batch < 1 || c.heads < 1) { *why = "batch and heads must be >= 1"; return TRA_ERR_INVALID_ARG; }
+  if (c.frames < 1 || c.height < 1 || c.width < 1) { *why = "frames, height and width must be >= 1"; return TRA_ERR_INVALID_ARG; }
+  if (c.frames > kMaxFrames) { *why = "frames > 64 is not supported"; return TRA_ERR_UNSUPPORTED; }
+  if (c.height > 1023 || c.width > 1023) { *why = "height and width must be <= 1023"; return TRA_ERR_UNSUPPORTED; }
+  if (c.tile_h < 1 || c.tile_w < 1) { *why = "tile_h and tile_w must be >= 1"; return TRA_ERR_INVALID_ARG; }
+  if (c.reserved != 0) { *why = "reserved must be 0"; return TRA_ERR_INVALID_ARG; }
+  if (c.dtype != TRA_BF16 && c.dtype != TRA_FP32) { *why = "unknown dtype"; return TRA_ERR_INVALID_ARG; }
+  if (c.rule != TRA_MASK_VOTE && c.rule != TRA_MASK_UNION) { *why = "unknown mask rule"; return TRA_ERR_INVALID_ARG; }
+  if (!(c.tau > 0.0 && c.tau < 1.0)) { *why = "tau must be in (0, 1)"; return TRA_ERR_INVALID_ARG; }
+  if (!(c.gamma >= 0.0) || !std::isfinite(c.gamma)) { *why = "gamma must be finite and >= 0"; return TRA_ERR_INVALID_ARG; }
+  if (c.head_dim != 64 && c.head_dim != 128) { *why = "head_dim must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
+  if (c.block != 64 && c.block != 128) { *why = "block must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
+  if (c.dtype == TRA_BF16 && c.block != 128) { *why = "bf16 needs block 128"; return TRA_ERR_UNSUPPORTED; }
+  const int64_t n = (int64_t)c.frames * c.height * c.width;
+  const int64_t nb = (n + c.block - 1) / c.block;
+  if (nb > kMaxBlocks) { *why = "more than 4096 blocks per head"; return TRA_ERR_UNSUPPORTED; }
+  const int64_t rows = (int64_t)c.batch * c.heads * nb;
+  if (rows * nb >= (int64_t)1 << 31 || (int64_t)c.batch * c.heads * n >= (int64_t)1 << 31) {
+    *why = "batch * heads * tokens too large for 32-bit indexing";
+    return TRA_ERR_UNSUPPORTED;
+  }
+  return TRA_OK;
+}
+
+void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
+                       bool with_thr, bool with_blocks) {
+  const int F = c.frames, H = c.height, W = c.width, b = c.block;
+  t->N = F * H * W;
+  t->NB = (t->N + b - 1) / b;
+  t->n_cap = (H - 1) * (H - 1) + (W - 1) * (W - 1);
+
+  std::vector<int32_t> perm;
+  if (with_perm_coord || with_blocks) {
+    // One frame's tile-major order, then offset per frame.
+    std::vector<int32_t> frame;
+    frame.reserve((size_t)H * W);
+    for (int ty = 0; ty < H; ty += c.tile_h)
+      for (int tx = 0; tx < W; tx += c.tile_w)
+        for (int x = ty; x < std::min(H, ty + c.tile_h); ++x)
+          for (int y = tx; y < std::min(W, tx + c.tile_w); ++y) frame.push_back(x * W + y);
+    perm.resize(t->N);
+    for (int f = 0; f < F; ++f)
+      for (int p = 0; p < H * W; ++p) perm[(size_t)f * H * W + p] = f * H * W + frame[p];
+  }
+  if (with_perm_coord) {
+    t->coord.resize(t->N);
+    for (int p = 0; p < t->N; ++p) {
+      const int i = perm[p];
+      t->coord[p] = pack_coord(i / (H * W), (i / W) % H, i % W);
+    }
+  }
+  if (with_thr) {
+    t->thr.resize((size_t)(t->n_cap + 1) * F);
+    for (int n = 0; n <= t->n_cap; ++n)
+      for (int d = 0; d < F; ++d) {
+        // n * exp(-2 gamma delta), floored.  delta = 0 gives n exactly.
+        const double e = std::exp(-2.0 * c.gamma * (double)d);
+        t->thr[(size_t)n * F + d] = d == 0 ? n : (int32_t)std::floor((double)n * e);
+      }
+  }
+  if (with_blocks) {
+    t->blocks.assign((size_t)t->NB * kBlockInfo, 0);
+    for (int u = 0; u < t->NB; ++u) {
+      int fmin = F, fmax = -1, xmin = H, xmax = -1, ymin = W, ymax = -1;
+      const int lo = u * b, hi = std::min(t->N, lo + b);
+      for (int p = lo; p < hi; ++p) {
+        const int i = perm[p];
+        const int f = i / (H * W), x = (i / W) % H, y = i % W;
+        fmin = std::min(fmin, f); fmax = std::max(fmax, f);
+        xmin = std::min(xmin, x); xmax = std::max(xmax, x);
+        ymin = std::min(ymin, y); ymax = std::max(ymax, y);
+      }
+      int32_t* o = &t->blocks[(size_t)u * kBlockInfo];
+      o[0] = fmin; o[1] = fmax; o[2] = xmin; o[3] = xmax; o[4] = ymin; o[5] = ymax;
+      o[6] = hi - lo; o[7] = 0;
+    }
+  }
+  if (with_perm_coord) t->perm = std::move(perm);
+}
+
+}  // namespace tra

@@ -1,0 +1,105 @@
+// Entropy -> budget -> squared radius, one thread per (batch, head, token).
+//
+//  K_hat = ceil(tau * exp(H))                       Sec. 3.1, Eq. 8 (fp64)
+//  C(n)  = sum_t #{(x', y') in frame : (x-x')^2 + (y-y')^2 <= thr[n][|t-f|]}
+//                                                   Sec. 3.2, Eq. 13
+//  n     = min{n in [0, n_cap] : C(n) >= K_hat}, else FULL        Eq. 14
+//
+// The paper tabulates the counts (App. C.1, a lookup table over query
+// coordinate and radius).  Here the counts are exact integer lattice counts
+// evaluated on the fly, row by row, so no per-shape count table has to live in
+// HBM; C(n) is non-decreasing in n, so the minimum is found by bisection.
+#include "tra_internal.h"
+
+namespace tra {
+namespace {
+
+// floor(sqrt(v)) for 0 <= v < 2^24, exact.
+__device__ __forceinline__ int isqrt_floor(int v) {
+  int r = (int)sqrtf((float)v);
+  while (r * r > v) --r;
+  while ((r + 1) * (r + 1) <= v) ++r;
+  return r;
+}
+
+// Lattice points (x', y') of an H x W frame with (x-x')^2 + (y-y')^2 <= T.
+__device__ int disk_count(int x, int y, int T, int H, int W) {
+  int w = isqrt_floor(T);                        // half-width of the row dx = 0
+  const int dx_end = min(w, max(x, H - 1 - x));  // rows beyond |dx| > sqrt(T) are empty
+  int total = 0;
+  for (int dx = 0; dx <= dx_end; ++dx) {
+    const int rem = T - dx * dx;
+    while (w * w > rem) --w;                     // half-width shrinks as |dx| grows
+    const int row = min(W - 1, y + w) - max(0, y - w) + 1;
+    if (x + dx <= H - 1) total += row;
+    if (dx > 0 && x - dx >= 0) total += row;
+  }
+  return total;
+}
+
+// C(n) of Eq. 13 for the query at (f, x, y).
+__device__ int grid_count(int f, int x, int y, int n, const int32_t* __restrict__ thr, int F,
+                          int H, int W) {
+  const int32_t* t = thr + (size_t)n * F;
+  int total = 0;
+  for (int d = 0; d < F; ++d) {
+    const int mult = (f - d >= 0) + (d > 0 && f + d <= F - 1);  // frames at distance d
+    if (mult == 0) break;                                       // no frame this far
+    const int T = t[d];
+    if (T == 0) {
+      // thr is non-increasing in d: every frame at distance >= d keeps only the
+      // query's own pixel position.
+      const int closer = min(f, d - 1) + min(F - 1 - f, d - 1) + 1;  // frames at distance < d (d >= 1 here)
+      total += F - (d == 0 ? 0 : closer);
+      break;
+    }
+    total += mult * disk_count(x, y, T, H, W);
+  }
+  return total;
+}
+
+__global__ __launch_bounds__(256) void budget_radius_kernel(
+    const float* __restrict__ entropy, int32_t* __restrict__ budget, int32_t* __restrict__ radius_sq,
+    const int32_t* __restrict__ thr, int total, int N, int F, int H, int W, int n_cap, double tau) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int i = idx % N;  // raster token
+  const double h = (double)entropy[idx];
+  const double kd = ceil(tau * exp(h));
+  int khat;
+  if (kd != kd || kd >= (double)N) khat = N;  // NaN entropy: keep everything
+  else if (kd < 1.0) khat = 1;
+  else khat = (int)kd;
+  if (budget) budget[idx] = khat;
+
+  const int f = i / (H * W), x = (i / W) % H, y = i % W;
+  int n;
+  if (khat <= F) {
+    n = 0;  // C(0) = F: the query's own position in every frame
+  } else if (grid_count(f, x, y, n_cap, thr, F, H, W) < khat) {
+    n = TRA_RADIUS_FULL;
+  } else {
+    int lo = 0, hi = n_cap;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (grid_count(f, x, y, mid, thr, F, H, W) >= khat) hi = mid;
+      else lo = mid + 1;
+    }
+    n = lo;
+  }
+  radius_sq[idx] = n;
+}
+
+}  // namespace
+
+hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
+                                int32_t* radius_sq, hipStream_t s) {
+  const int total = p.cfg.batch * p.cfg.heads * p.N;
+  const int threads = 256;
+  hipLaunchKernelGGL(budget_radius_kernel, dim3((total + threads - 1) / threads), dim3(threads), 0, s,
+                     entropy, budget, radius_sq, p.d_thr, total, p.N, p.cfg.frames, p.cfg.height,
+                     p.cfg.width, p.n_cap, p.cfg.tau);
+  return hipGetLastError();
+}
+
+}  // namespace tra

@@ -1,0 +1,87 @@
+// Internal declarations shared by the TRA library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "tra.h"
+
+namespace tra {
+
+// Packed token coordinate of a tile-major position: y in bits 0-9, x in bits
+// 10-19, f in bits 20-25 (the plan limits W, H <= 1023 and F <= 64).
+__host__ __device__ inline int32_t pack_coord(int f, int x, int y) {
+  return (f << 20) | (x << 10) | y;
+}
+__host__ __device__ inline int coord_f(int32_t c) { return c >> 20; }
+__host__ __device__ inline int coord_x(int32_t c) { return (c >> 10) & 1023; }
+__host__ __device__ inline int coord_y(int32_t c) { return c & 1023; }
+
+constexpr int kBlockInfo = 8;  // f_min f_max x_min x_max y_min y_max n_valid 0
+constexpr int kMaxFrames = 64;
+constexpr int kMaxBlocks = 4096;
+constexpr int kSortChunk = 256;
+
+// Host-side tables of one shape (plan.cpp).
+struct HostTables {
+  int32_t N = 0, NB = 0, n_cap = 0;
+  std::vector<int32_t> perm;    // [N] tile-major position -> raster index
+  std::vector<int32_t> coord;   // [N] packed (f, x, y) of tile-major position
+  std::vector<int32_t> thr;     // [(n_cap + 1) * F]
+  std::vector<int32_t> blocks;  // [NB * kBlockInfo]
+};
+
+// Validates the config; on failure returns the status and fills `why`.
+tra_status validate_config(const tra_config* cfg, std::string* why);
+void build_host_tables(const tra_config& cfg, HostTables* t, bool with_perm_coord,
+                       bool with_thr, bool with_blocks);
+
+}  // namespace tra
+
+struct tra_plan_s {
+  tra_config cfg;
+  int device = 0;
+  int32_t N = 0, NB = 0, n_cap = 0, rows = 0;
+  int32_t* d_perm = nullptr;
+  int32_t* d_coord = nullptr;
+  int32_t* d_thr = nullptr;
+  int32_t* d_blocks = nullptr;
+  int32_t* d_sort_ws = nullptr;  // counting-sort workspace of the row order
+  int64_t sort_ws_elems = 0;
+  int32_t sort_chunks = 0;
+};
+
+namespace tra {
+
+// ----------------------------------------------------------- kernel launchers
+// Each returns hipSuccess or the launch error.  All run on `stream`.
+
+// Attention family.  mode flags select the variant.
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  float* entropy;
+  const int32_t* cnt;    // sparse only
+  const int32_t* cols;   // sparse only
+  const int32_t* order;  // sparse only, may be null
+  bool sparse;
+};
+hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_f32(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
+
+hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
+                                int32_t* radius_sq, hipStream_t s);
+
+hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask,
+                             int32_t* cnt, int32_t* cols, hipStream_t s);
+
+hipError_t launch_row_order(const tra_plan_s& p, const int32_t* cnt, int32_t* order,
+                            hipStream_t s);
+
+}  // namespace tra

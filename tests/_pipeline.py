@@ -1,0 +1,208 @@
+"""Shared helpers for the GPU tests: run the library's path on a workload and
+compute the oracle's answer on sampled query blocks."""
+from __future__ import annotations
+
+import math
+import sys
+import time
+
+import numpy as np
+
+import oracle as O
+import paper_2608_02504_amd as tra
+import synth
+
+TOL_O_BF16 = 2e-2      # max-abs on attention outputs, bf16 I/O
+TOL_O_FP32 = 1e-5      # max-abs on attention outputs, fp32 I/O
+TOL_H_REL = 1e-3       # entropy: |dH| <= max(1e-3 |H|, 1e-4) nats
+TOL_H_ABS = 1e-4
+
+
+def log(msg):
+    sys.stdout.write(f"[tra-test {time.strftime('%H:%M:%S')}] {msg}\n")
+    sys.stdout.flush()
+
+
+def torch_inputs(w, q, k, v, device="cuda"):
+    import torch
+    if w.dtype == "bf16":
+        conv = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(device)
+    else:
+        conv = lambda a: torch.from_numpy(a).to(device)
+    return conv(q), conv(k), conv(v)
+
+
+def to_np_f64(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy().astype(np.float64)
+
+
+class Run:
+    """All stage outputs of one pass of the path on the GPU."""
+
+    def __init__(self, w, rule="vote", with_order=True, inputs=None, radius_override=None):
+        import torch
+        self.w = w
+        self.cfg = tra.Config.from_workload(w, rule=rule)
+        self.plan = tra.Plan(self.cfg)
+        log(f"workload {w.name} N={w.n_tokens} heads={w.heads} d={w.head_dim} {w.dtype} rule={rule}")
+        if inputs is None:
+            inputs = synth.generate(w)
+        self.q_np, self.k_np, self.v_np = inputs
+        q, k, v = torch_inputs(w, *inputs)
+        B, Ha, N, d = q.shape
+        NB = self.plan.n_blocks
+        dev = q.device
+        f32, i32 = torch.float32, torch.int32
+        self.H = torch.empty(B, Ha, N, dtype=f32, device=dev)
+        self.H_only = torch.empty_like(self.H)
+        self.O_ent = torch.empty_like(q)
+        self.budget = torch.empty(B, Ha, N, dtype=i32, device=dev)
+        self.rad = torch.empty(B, Ha, N, dtype=i32, device=dev)
+        self.mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
+        self.cnt = torch.empty(B, Ha, NB, dtype=i32, device=dev)
+        self.cols = torch.empty(B, Ha, NB, NB, dtype=i32, device=dev)
+        self.order = torch.empty(B * Ha * NB, dtype=i32, device=dev) if with_order else None
+        self.O_sp = torch.empty_like(q)
+        self.lse_sp = torch.empty(B, Ha, N, dtype=f32, device=dev)
+        self.O_d = torch.empty_like(q)
+        self.lse_d = torch.empty(B, Ha, N, dtype=f32, device=dev)
+
+        tra.tra_entropy(self.plan, q, k, v, self.O_ent, self.H)
+        tra.tra_entropy(self.plan, q, k, None, None, self.H_only)
+        tra.tra_budget_radius(self.plan, self.H, self.budget, self.rad)
+        if radius_override is not None:
+            self.rad.fill_(int(radius_override))
+        tra.tra_build_block_mask(self.plan, self.rad, self.mask, self.cnt, self.cols, self.order)
+        tra.tra_sparse_attention(self.plan, q, k, v, self.cnt, self.cols, self.order, self.O_sp,
+                                 self.lse_sp)
+        tra.tra_dense_attention(self.plan, q, k, v, self.O_d, self.lse_d)
+        torch.cuda.synchronize()
+        self.q, self.k, self.v = q, k, v
+        log(f"workload {w.name}: GPU path done")
+
+    def np(self, name):
+        t = getattr(self, name)
+        if t.dtype.is_floating_point:
+            return to_np_f64(t)
+        return t.cpu().numpy()
+
+
+def sample_blocks(w, n_blocks_per_head: int, seed: int):
+    """Seeded query blocks per (batch, head); always includes the ragged last block."""
+    rng = np.random.default_rng(seed)
+    nb = w.n_blocks
+    out = {}
+    for b in range(w.batch):
+        for h in range(w.heads):
+            if n_blocks_per_head >= nb:
+                sel = np.arange(nb)
+            else:
+                sel = np.unique(np.concatenate([rng.choice(nb - 1, n_blocks_per_head - 1, replace=False),
+                                                [nb - 1]]))
+            out[(b, h)] = sel
+    return out
+
+
+class OracleTables:
+    def __init__(self, w):
+        self.F, self.H, self.W = w.frames, w.height, w.width
+        self.ncap = O.n_cap(w.height, w.width)
+        self.thr = O.threshold_table(self.ncap, w.frames, w.gamma)
+        self.disk = O.disk_count_table(w.height, w.width, self.ncap)
+        self.perm = O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w)
+        self.f, self.x, self.y = O.grid_coords(w.frames, w.height, w.width)
+
+
+def check_head(run: Run, tabs: OracleTables, b: int, h: int, blocks, tol_o: float, report: dict):
+    """Compare every stage for the sampled query blocks of one (batch, head)."""
+    import torch
+    w = run.w
+    N, bs = w.n_tokens, w.block
+    perm = tabs.perm
+    q = synth.to_f64(run.q_np[b, h], w.dtype)
+    k = synth.to_f64(run.k_np[b, h], w.dtype)
+    v = synth.to_f64(run.v_np[b, h], w.dtype)
+    rows = np.concatenate([perm[u * bs:min((u + 1) * bs, N)] for u in blocks])
+
+    # entropy and dense output (Eq. 1, Eq. 2), one score matrix for all rows
+    s = O.scores(q[rows], k)
+    p = O.softmax_rows(s)
+    H_ref = O.entropy_from_probs(p)
+    O_ref = (p @ torch.as_tensor(v)).numpy()
+    lse_ref = (torch.logsumexp(s, dim=1)).numpy()
+    del s, p
+    H_gpu = run.H[b, h].double().cpu().numpy()[rows]
+    dH = np.abs(H_gpu - H_ref)
+    assert (dH <= np.maximum(TOL_H_REL * np.abs(H_ref), TOL_H_ABS)).all(), \
+        f"entropy: max |dH| {dH.max():.3e} at H={H_ref[dH.argmax()]:.4f}"
+    H_only = run.H_only[b, h].cpu().numpy()[rows]
+    assert np.array_equal(H_only, run.H[b, h].cpu().numpy()[rows]), "entropy-only != fused entropy"
+    O_d = to_np_f64(run.O_d[b, h])[rows]
+    errd = np.abs(O_d - O_ref).max()
+    assert errd <= tol_o, f"dense output max-abs {errd:.3e}"
+    lse_d = run.lse_d[b, h].double().cpu().numpy()[rows]
+    assert np.abs(lse_d - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "dense lse"
+    report["max_dH"] = max(report.get("max_dH", 0.0), float(dH.max()))
+    report["max_err_dense"] = max(report.get("max_err_dense", 0.0), float(errd))
+
+    # budget and radius from the GPU's fp32 entropy (Eqs. 8, 13, 14): bit-exact
+    khat_ref = O.token_budget(H_gpu, w.tau, N)
+    t = w.tau * np.exp(H_gpu)
+    near = np.abs(t - np.round(t)) <= 1e-12 * np.maximum(t, 1.0)
+    report["near_integer_budgets"] = report.get("near_integer_budgets", 0) + int(near.sum())
+    kh_gpu = run.budget[b, h].cpu().numpy()[rows]
+    assert np.array_equal(kh_gpu[~near], khat_ref[~near]), "budget mismatch"
+    n_ref = O.select_radius(kh_gpu, tabs.f[rows], tabs.x[rows], tabs.y[rows], tabs.F, tabs.thr, tabs.disk)
+    n_gpu = run.rad[b, h].cpu().numpy()[rows]
+    assert np.array_equal(n_gpu, n_ref), f"radius mismatch at {np.nonzero(n_gpu != n_ref)[0][:5]}"
+
+    # block mask rows (Alg. 1) from the GPU radii: bit-exact
+    n_full = run.rad[b, h].cpu().numpy()
+    M_ref = O.block_mask_rows(n_full, perm, bs, tabs.F, tabs.H, tabs.W, w.gamma, list(blocks),
+                              rule=run.cfg.rule)
+    M_gpu = run.mask[b, h].cpu().numpy()[blocks].astype(bool)
+    assert np.array_equal(M_gpu, M_ref), f"mask mismatch in blocks {np.nonzero((M_gpu != M_ref).any(1))[0][:5]}"
+
+    # block-sparse attention (Eq. 16 at block granularity)
+    r2, O_ms, lse_ms = O.masked_attention_rows(q, k, v, perm, bs, list(blocks), M_ref, return_lse=True)
+    assert np.array_equal(r2, rows)
+    O_s = to_np_f64(run.O_sp[b, h])[rows]
+    errs = np.abs(O_s - O_ms).max()
+    assert errs <= tol_o, f"sparse output max-abs {errs:.3e}"
+    lse_s = run.lse_sp[b, h].double().cpu().numpy()[rows]
+    assert np.abs(lse_s - lse_ms).max() <= 1e-4 + 1e-5 * np.abs(lse_ms).max(), "sparse lse"
+    report["max_err_sparse"] = max(report.get("max_err_sparse", 0.0), float(errs))
+    return M_ref
+
+
+def check_lists(run: Run):
+    """cnt / cols / order agree with the mask for every row (integer, exact)."""
+    mask = run.mask.cpu().numpy().astype(bool)
+    cnt = run.cnt.cpu().numpy()
+    cols = run.cols.cpu().numpy()
+    B, Ha, NB, _ = mask.shape
+    m2 = mask.reshape(-1, NB)
+    c2 = cols.reshape(-1, NB)
+    n2 = cnt.reshape(-1)
+    assert np.array_equal(n2, m2.sum(axis=1))
+    for r in range(m2.shape[0]):
+        nz = np.nonzero(m2[r])[0]
+        assert np.array_equal(c2[r, :n2[r]], nz)
+        assert (c2[r, n2[r]:] == -1).all()
+    if run.order is not None:
+        order = run.order.cpu().numpy()
+        assert np.array_equal(np.sort(order), np.arange(m2.shape[0]))
+        w = n2[order]
+        assert (np.diff(w) <= 0).all()
+        ties = np.diff(w) == 0
+        assert (np.diff(order)[ties] > 0).all()
+    # diagonal always retained
+    idx = np.arange(NB)
+    assert mask[:, :, idx, idx].all()
+
+
+def retained_fraction(run: Run):
+    return O.retained_fraction(run.mask.cpu().numpy().astype(bool), run.w.n_tokens, run.w.block)

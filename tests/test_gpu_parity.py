@@ -1,0 +1,175 @@
+"""GPU parity of every stage of the path against the CPU oracle, through the
+C ABI.  Bars: radii, budgets, masks and lists bit-exact; entropy within
+max(1e-3 |H|, 1e-4) nats; attention outputs within 2e-2 max-abs (bf16 I/O) or
+1e-5 (fp32 I/O)."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from _pipeline import (TOL_O_BF16, TOL_O_FP32, OracleTables, Run, check_head, check_lists, log,
+                       retained_fraction, sample_blocks)
+
+pytestmark = pytest.mark.gpu
+
+BLOCKS_PER_HEAD = int(os.environ.get("TRA_TEST_BLOCKS", "32"))
+
+
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+# Small workloads the oracle checks completely: several tiles, ragged tails.
+SMALL = {
+    "tiny": synth.workload("tiny"),
+    "tiny_union": synth.workload("tiny"),
+    "ragged_fp32_d128_b128": synth.Workload("ragged_fp32_d128_b128", 1, 2, 128, "fp32", 3, 7, 19, 128,
+                                            0.25, 4.0, 0.6, seed=77, tile_h=8, tile_w=16),
+    "ragged_bf16_d128": synth.Workload("ragged_bf16_d128", 1, 2, 128, "bf16", 4, 13, 37, 128,
+                                       0.25, 4.0, 0.6, seed=78, tile_h=8, tile_w=16),
+    "ragged_bf16_d64": synth.Workload("ragged_bf16_d64", 2, 2, 64, "bf16", 3, 11, 29, 128,
+                                      0.1, 8.0, 0.95, seed=79, tile_h=8, tile_w=16),
+    "aligned_bf16": synth.Workload("aligned_bf16", 1, 2, 128, "bf16", 5, 16, 32, 128,
+                                   0.25, 4.0, 0.6, seed=80, tile_h=8, tile_w=16),
+    "single_token": synth.Workload("single_token", 1, 1, 128, "bf16", 1, 1, 1, 128,
+                                   0.25, 4.0, 0.6, seed=81, tile_h=8, tile_w=16),
+    "fp32_b64_d128": synth.Workload("fp32_b64_d128", 1, 1, 128, "fp32", 2, 9, 11, 64,
+                                    0.25, 4.0, 0.6, seed=82, tile_h=8, tile_w=8),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_full_parity(name):
+    _gpu()
+    w = SMALL[name]
+    rule = "union" if name.endswith("union") else "vote"
+    run = Run(w, rule=rule)
+    tabs = OracleTables(w)
+    tol = TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
+    report = {}
+    for b in range(w.batch):
+        for h in range(w.heads):
+            check_head(run, tabs, b, h, np.arange(w.n_blocks), tol, report)
+    check_lists(run)
+    log(f"{name}: rho={retained_fraction(run):.4f} {report}")
+    assert report["near_integer_budgets"] == 0
+
+
+def test_single_token_closed_form():
+    """N = 1: the only key has p = 1, so H = 0, o = v, radius 0, mask [[1]]."""
+    _gpu()
+    run = Run(SMALL["single_token"])
+    assert abs(float(run.H[0, 0, 0])) < 1e-6
+    assert int(run.rad[0, 0, 0]) == 0 and int(run.cnt[0, 0, 0]) == 1
+    assert np.array_equal(run.np("O_sp")[0, 0], synth.to_f64(run.v_np[0, 0], "bf16"))
+    assert np.array_equal(run.np("O_d")[0, 0], synth.to_f64(run.v_np[0, 0], "bf16"))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_entropy_closed_forms(dtype):
+    """Uniform scores -> H = log N; one dominant key -> H = 0 (Eq. 2 bounds)."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    w = synth.Workload("cf", 1, 2, 128, dtype, 2, 12, 20, 128, 0.25, 4.0, 0.6, tile_h=8, tile_w=16)
+    cfg = tra.Config.from_workload(w)
+    plan = tra.Plan(cfg)
+    N, d = w.n_tokens, 128
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q = torch.randn(1, 2, N, d, generator=torch.Generator().manual_seed(0)).to(tdt).cuda()
+    k = torch.zeros(1, 2, N, d, dtype=tdt, device="cuda")
+    k[:, :, :] = torch.randn(d, generator=torch.Generator().manual_seed(1)).to(tdt).cuda()
+    k[:, 1] = 0.0
+    q[:, 1] = 0.0
+    q[:, 1, :, 0] = 1.0
+    k[:, 1, 123, 0] = 64.0 * math.sqrt(d)    # key 123 leads every other score by 64
+    H = torch.empty(1, 2, N, device="cuda")
+    tra.tra_entropy(plan, q, k, None, None, H)
+    torch.cuda.synchronize()
+    Hn = H.cpu().numpy()
+    assert np.abs(Hn[0, 0] - math.log(N)).max() < 1e-4 * math.log(N)
+    assert np.abs(Hn[0, 1]).max() < 1e-4
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny"])
+def test_full_radius_sparse_equals_dense_bitwise(name):
+    """All radii FULL -> every block retained -> the sparse kernel walks the
+    same key blocks in the same order as the dense one: bitwise equal."""
+    _gpu()
+    run = Run(SMALL[name], radius_override=2 ** 31 - 1)
+    assert run.mask.all()
+    import torch
+    assert torch.equal(run.O_sp, run.O_d)
+    assert torch.equal(run.lse_sp, run.lse_d)
+    # the fused warm-up output of the entropy pass is the dense output too
+    assert torch.equal(run.O_ent, run.O_d)
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny"])
+def test_zero_radius_is_block_diagonal(name):
+    """All radii 0 -> (vote) only the diagonal block survives -> block-diagonal
+    attention, i.e. textbook attention inside each block."""
+    _gpu()
+    w = SMALL[name]
+    run = Run(w, radius_override=0)
+    m = run.mask.cpu().numpy()
+    eye = np.broadcast_to(np.eye(w.n_blocks, dtype=np.uint8), m.shape)
+    assert np.array_equal(m, eye)
+    tabs = OracleTables(w)
+    tol = TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
+    perm = tabs.perm
+    for h in range(w.heads):
+        q, k, v = (synth.to_f64(a[0, h], w.dtype) for a in (run.q_np, run.k_np, run.v_np))
+        O_gpu = run.np("O_sp")[0, h]
+        for u in range(w.n_blocks):
+            idx = perm[u * w.block:min((u + 1) * w.block, w.n_tokens)]
+            want = O.dense_attention(q[idx], k[idx], v[idx])
+            assert np.abs(O_gpu[idx] - want).max() <= tol
+
+
+def test_determinism_bitwise():
+    _gpu()
+    import torch
+    w = SMALL["ragged_bf16_d64"]
+    inputs = synth.generate(w)
+    a, b = Run(w, inputs=inputs), Run(w, inputs=inputs)
+    for name in ("H", "H_only", "O_ent", "budget", "rad", "mask", "cnt", "cols", "order", "O_sp",
+                 "lse_sp", "O_d", "lse_d"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+
+
+def _sampled(name, heads=None):
+    _gpu()
+    w = synth.workload(name)
+    run = Run(w)
+    tabs = OracleTables(w)
+    report = {}
+    samples = sample_blocks(w, BLOCKS_PER_HEAD, seed=2024)
+    check_lists(run)
+    for (b, h), blocks in samples.items():
+        if heads is not None and h not in heads:
+            continue
+        check_head(run, tabs, b, h, blocks, TOL_O_BF16, report)
+    rho = retained_fraction(run)
+    log(f"{name}: rho={rho:.4f} sampled {BLOCKS_PER_HEAD} blocks/head {report}")
+    assert report["near_integer_budgets"] == 0
+    return run
+
+
+def test_wan13b_480p_sampled():
+    _sampled("wan13b_480p")
+
+
+@pytest.mark.slow
+def test_wan14b_720p_sampled():
+    _sampled("wan14b_720p")
+
+
+@pytest.mark.slow
+def test_hunyuan_720p_sampled():
+    _sampled("hunyuan_720p")

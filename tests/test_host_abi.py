@@ -1,0 +1,100 @@
+"""CPU tests of the C ABI: the library loads, exports every declared symbol,
+its host-side tables agree with the oracle's independent ones, and bad
+arguments come back as status codes (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2608_02504_amd as tra
+import synth
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "tra.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tra_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = tra.lib()
+    declared = _declared_functions()
+    assert set(declared) == set(tra.EXPORTED_SYMBOLS)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert "gfx950" in tra.tra_version()
+
+
+@pytest.mark.parametrize("name", ["tiny", "wan13b_480p", "wan14b_720p", "hunyuan_720p"])
+def test_host_tables_match_oracle(name):
+    w = synth.workload(name)
+    cfg = tra.Config.from_workload(w)
+    perm, thr, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    assert ncap == O.n_cap(w.height, w.width)
+    assert np.array_equal(perm, O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w))
+    assert np.array_equal(thr, O.threshold_table(ncap, w.frames, w.gamma))
+    f, x, y = O.grid_coords(w.frames, w.height, w.width)
+    for u, (lo, hi) in enumerate(O.block_bounds(w.n_tokens, w.block)):
+        r = perm[lo:hi]
+        want = [f[r].min(), f[r].max(), x[r].min(), x[r].max(), y[r].min(), y[r].max(), hi - lo, 0]
+        assert list(blocks[u]) == want, u
+
+
+def test_tiny_layout_sizes():
+    cfg = tra.Config.from_workload(synth.workload("wan14b_720p"))
+    assert cfg.n_tokens == 75600 and cfg.n_blocks == 591
+    cfg3 = tra.Config.from_workload(synth.workload("hunyuan_720p"))
+    assert cfg3.n_tokens == 118800 and cfg3.n_blocks == 929
+    assert cfg3.n_tokens - (cfg3.n_blocks - 1) * 128 == 16
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(head_dim=96), 2), (dict(block=32), 2), (dict(block=64), 2),   # bf16 needs block 128
+    (dict(frames=0), 1), (dict(frames=65), 2), (dict(height=2000), 2),
+    (dict(tau=1.0), 1), (dict(tau=0.0), 1), (dict(gamma=-0.1), 1),
+    (dict(gamma=float("nan")), 1), (dict(tile_h=0), 1), (dict(dtype="fp16"), 1),
+    (dict(rule="maj"), 1), (dict(batch=0), 1),
+])
+def test_invalid_configs_rejected(change, status):
+    base = dict(batch=1, heads=2, frames=3, height=8, width=16, head_dim=128)
+    base.update(change)
+    cfg = tra.Config(**base)
+    with pytest.raises(tra.TraError) as ei:
+        tra.tra_plan_host_tables(cfg)
+    assert ei.value.status == status
+
+
+def test_fp32_block64_accepted_host_side():
+    cfg = tra.Config(batch=1, heads=1, frames=2, height=8, width=8, head_dim=64, block=64,
+                     tile_h=8, tile_w=8, dtype="fp32")
+    perm, thr, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    assert ncap == 98 and thr.shape == (99, 2) and blocks.shape == (2, 8)
+
+
+def test_null_arguments_are_errors_not_crashes():
+    L = tra.lib()
+    assert L.tra_plan_host_tables(None, None, None, None, None) == 1
+    assert L.tra_plan_create(None, None) == 1
+    assert L.tra_entropy(None, None, None, None, None, None, None) == 1
+    assert L.tra_budget_radius(None, None, None, None, None) == 1
+    assert L.tra_build_block_mask(None, None, None, None, None, None, None) == 1
+    assert L.tra_sparse_attention(None, None, None, None, None, None, None, None, None, None) == 1
+    assert L.tra_dense_attention(None, None, None, None, None, None, None) == 1
+    assert b"NULL" in L.tra_last_error()
+    assert L.tra_plan_destroy(None) == 0
+    assert L.tra_last_error() == b""
+
+
+def test_plan_create_without_gpu_reports_device_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    cfg = tra.Config.from_workload(synth.workload("tiny"))
+    with pytest.raises(tra.TraError) as ei:
+        tra.Plan(cfg)
+    assert ei.value.status in (2, 3)
