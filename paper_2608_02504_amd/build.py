@@ -23,6 +23,9 @@ COMMON = [
     f"-I{INCLUDE}", f"-I{CSRC}",
     # packed fp32 VALU ops stay off: the compiler emits only scalar-lane fp32 ops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in architectural VGPRs: the softmax reads every score with
+    # VALU instructions, which cannot address accumulation registers
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -105,6 +105,8 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_thr);
   (void)hipFree(p->d_blocks);
   (void)hipFree(p->d_sort_ws);
+  (void)hipFree(p->d_kt);
+  (void)hipFree(p->d_vt);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -140,6 +142,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
     p->sort_chunks = (p->rows + tra::kSortChunk - 1) / tra::kSortChunk;
     // chunk histograms over keys 0..NB, plus one total slot
     p->sort_ws_elems = (int64_t)(t.NB + 1) * p->sort_chunks + 1;
+    p->n_pad = t.NB * cfg->block;
 
     auto upload = [&](int32_t** dst, const std::vector<int32_t>& src) -> hipError_t {
       hipError_t err = hipMalloc((void**)dst, src.size() * sizeof(int32_t));
@@ -153,6 +156,14 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
         (e = hipMalloc((void**)&p->d_sort_ws, p->sort_ws_elems * sizeof(int32_t))) != hipSuccess) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
+    }
+    if (cfg->dtype == TRA_BF16) {
+      const size_t bytes = (size_t)cfg->batch * cfg->heads * p->n_pad * cfg->head_dim * sizeof(uint16_t);
+      if ((e = hipMalloc((void**)&p->d_kt, bytes)) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_vt, bytes)) != hipSuccess) {
+        tra_plan_destroy(p);
+        return fail(TRA_ERR_ALLOC, std::string("plan K/V workspace: ") + hipGetErrorString(e));
+      }
     }
     *out = p;
     return ok();

@@ -52,6 +52,11 @@ struct tra_plan_s {
   int32_t* d_sort_ws = nullptr;  // counting-sort workspace of the row order
   int64_t sort_ws_elems = 0;
   int32_t sort_chunks = 0;
+  // bf16 plans: K and V gathered into tile-major order, [batch*heads][NB*block][d],
+  // rows past N zero-filled, so the attention loop addresses tiles affinely.
+  int32_t n_pad = 0;
+  uint16_t* d_kt = nullptr;
+  uint16_t* d_vt = nullptr;
 };
 
 namespace tra {
