@@ -10,18 +10,18 @@
 //   the same permutation inside the kernel, so callers keep raster order.
 //
 // Work decomposition
-//   One workgroup (4 waves, 256 threads, one wave per SIMD, up to 512 VGPRs a
-//   wave) per query-block row r = (b, h, u): 128 queries, wave w owning
-//   queries [32w, 32w + 32).  It walks the key blocks of its row (all NB for
-//   dense; cols[r][0..cnt[r]) for sparse), 128 keys per tile.
+//   One workgroup (4 waves, 256 threads) per query-block row r = (b, h, u):
+//   128 queries, wave w owning queries [32w, 32w + 32).  It walks the key
+//   blocks of its row (all NB for dense; cols[r][0..cnt[r]) for sparse), 128
+//   keys per tile.  Two workgroups share a CU (64 KB of LDS each), so every
+//   SIMD runs one workgroup's matrix phase while the other is in its softmax.
 //
-// Pipeline (per tile i, one barrier)
-//   K and V tiles go from HBM straight into LDS (global_load_lds_dwordx4),
-//   double-buffered, issued one full tile ahead: at the top of tile i the
-//   loads of K_{i+2} and V_{i+1} start.  Then, in one straight-line block,
-//   the matrix cores compute S_{i+1} = K_{i+1} Q^T while the VALU runs the
-//   softmax of S_i; then O += V_i P_i.  16-byte LDS chunks are XOR-swizzled
-//   per row so K reads and transposed V reads hit every bank once.
+// Per tile (split barriers)
+//   K and V go from HBM straight into LDS (global_load_lds_dwordx4, no register
+//   staging), 16-byte chunks XOR-swizzled per row so K reads and transposed V
+//   reads hit every bank once.  The next K tile streams in during softmax + PV,
+//   the next V tile during QK^T + softmax.  Scheduling hints keep several LDS
+//   operand reads in flight ahead of the MFMAs.
 //
 // Matrix work (v_mfma_f32_32x32x16_bf16, fp32 accumulation)
 //   S^T = K Q^T: keys are the M side and the wave's 32 queries the N side, so a
@@ -144,17 +144,37 @@ __device__ __forceinline__ void qk_step(f32x16& s, const lds_u8* kbuf, const uin
   s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s, 0, 0, 0);
 }
 
+// Scheduling pattern for a run of n MFMAs each fed by `reads` LDS reads: the
+// first `ahead` MFMAs' operands are requested up front, then every MFMA is
+// followed by the reads of the MFMA `ahead` places later, so LDS latency hides
+// behind matrix work.
+template <int n, int reads, int ahead>
+__device__ __forceinline__ void sched_reads_ahead() {
+#pragma unroll
+  for (int i = 0; i < ahead; ++i) __builtin_amdgcn_sched_group_barrier(0x100, reads, 0);
+#pragma unroll
+  for (int i = 0; i < n - ahead; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, reads, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < ahead; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+}
+
 template <int D>
 __device__ __forceinline__ void qk_tile(f32x16 (&s)[4], const lds_u8* kbuf,
                                         const uint32_t (&koff)[Geo<D>::QK_STEPS],
                                         const bf16x8 (&qf)[Geo<D>::QK_STEPS]) {
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
+  for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
+  // k-step outer, sub-tile inner: four independent accumulation chains
 #pragma unroll
-    for (int kk = 0; kk < Geo<D>::QK_STEPS; ++kk) qk_step<D>(s[kt], kbuf, koff, qf, kt, kk);
-  }
+  for (int kk = 0; kk < Geo<D>::QK_STEPS; ++kk)
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) qk_step<D>(s[kt], kbuf, koff, qf, kt, kk);
+  sched_reads_ahead<4 * Geo<D>::QK_STEPS, 1, 4>();
 }
 
 // Keys past the end of a ragged last block get a large finite negative score:
@@ -230,33 +250,36 @@ __device__ __forceinline__ void pv_step(f32x16& oacc, const lds_u8* vbuf, const 
                                                  __builtin_bit_cast(bf16x8, bw), oacc, 0, 0, 0);
 }
 
-template <int D, bool SPARSE, bool PV, bool ENT>
-__global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
+// Main attention kernel.  One workgroup per query-block row, two workgroups per
+// CU (64 KB of LDS each: one K and one V tile).  Split barriers let the next
+// K tile stream in during softmax + PV and the next V tile during QK^T +
+// softmax; each SIMD interleaves one workgroup's matrix phase with the other's
+// vector phase.  OCC is the workgroups-per-CU bound the registers are sized
+// for (the fused entropy + output variant needs one per CU to avoid spills).
+template <int D, bool SPARSE, bool PV, bool ENT, int OCC>
+__global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
     const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ lse,
     float* __restrict__ entropy, const int32_t* __restrict__ perm, const int32_t* __restrict__ cnt,
     const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N, int n_pad, int NB,
     int rows, float scale_log2) {
   using G = Geo<D>;
-  constexpr int TILE = kBK * D * 2;  // bytes of one K or V tile
-  // [K0][K1][V0][V1]
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[(PV ? 4 : 2) * TILE];
+  constexpr int TILE = kBK * D * 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[(PV ? 2 : 1) * TILE];  // [K][V]
   lds_u8* lds = (lds_u8*)smem;
 
   int r = blockIdx.x;
   if (SPARSE && order) {
     r = order[blockIdx.x];
-    if (r < 0 || r >= rows) return;  // whole workgroup leaves together
+    if (r < 0 || r >= rows) return;
   }
   const int bh = r / NB, u = r - bh * NB;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int col = lane & 31;   // query column of this lane within the wave
-  const int half = lane >> 5;  // lane half: selects k-slots / output rows
+  const int col = lane & 31, half = lane >> 5;
   const size_t head_off = (size_t)bh * N * D;
   const uint16_t* Kb = ktile + (size_t)bh * n_pad * D;
   const uint16_t* Vb = vtile + (size_t)bh * n_pad * D;
 
-  // ---- Q fragments: B operand of S^T = K Q^T, 8 bf16 per lane per 16-deep step
   const int qpos = u * kBQ + wave * 32 + col;
   const bool qvalid = qpos < N;
   const int qrow = qvalid ? perm[qpos] : 0;
@@ -269,18 +292,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
       qf[kk] = __builtin_bit_cast(bf16x8, x);
     }
   }
-
-  // ---- per-lane LDS byte offsets (sub-tile, k-step and buffer terms are immediates)
   uint32_t koff[G::QK_STEPS];
   {
-    const int sw = swz<G::CH>(col);  // key 32kt + col has the same swizzle for every kt
+    const int sw = swz<G::CH>(col);
 #pragma unroll
     for (int kk = 0; kk < G::QK_STEPS; ++kk) koff[kk] = col * D * 2 + (((2 * kk + half) ^ sw) << 4);
   }
   uint32_t voff[2][G::D_TILES];
   {
     const int grp = lane >> 4, j = lane & 15;
-    const int kj = 4 * half + (j >> 2);  // key offset inside a 16-key step
+    const int kj = 4 * half + (j >> 2);
     const int dq = 16 * (grp & 1) + 4 * (j & 3);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -296,7 +317,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
 
   const int count = SPARSE ? min(max(cnt[r], 0), NB) : NB;
   const int32_t* colp = SPARSE ? cols + (size_t)r * NB : nullptr;
-  // key block of list entry i (ids outside [0, NB) are clamped into range)
   auto blk = [&](int i) -> int { return SPARSE ? min(max(colp[i], 0), NB - 1) : i; };
 
   f32x16 oacc[PV ? G::D_TILES : 1];
@@ -307,58 +327,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
   RowState st{-INFINITY, 0.f, 0.f};
 
   if (count > 0) {
-    f32x16 s[4];
-    uint32_t pb[32];
-    // ---- prologue: K_0, V_0, K_1 in flight; S_0 = K_0 Q^T and its max
     int b_cur = blk(0);
-    issue_tile<D>((uint16_t*)(smem + 0 * TILE), Kb + (size_t)b_cur * kBK * D, wave, lane);
-    if (PV) issue_tile<D>((uint16_t*)(smem + 2 * TILE), Vb + (size_t)b_cur * kBK * D, wave, lane);
-    int b_next = count > 1 ? blk(1) : 0;
-    if (count > 1) {
-      issue_tile<D>((uint16_t*)(smem + 1 * TILE), Kb + (size_t)b_next * kBK * D, wave, lane);
-      wait_vm<(PV ? 2 : 1) * G::LPT>();
-    } else {
-      wait_vm<(PV ? 1 : 0) * G::LPT>();
-    }
-    __syncthreads();
-    qk_tile<D>(s, lds + 0 * TILE, koff, qf);
-    if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
-    float sc = tile_max<ENT>(s, scale_log2, st);
-
-    // One pipeline step on tile i: S_i (already max-folded) in s, K_{i+1} in
-    // buffer KN, V_i in buffer VC.  Buffers KF / VF (tile i-1) take K_{i+2} / V_{i+1}.
-    auto step = [&](int i, auto KN, auto VC) {
-      constexpr int kn = decltype(KN)::value, kf = 1 - kn;
-      constexpr int vc = decltype(VC)::value, vf = 1 - vc;
-      wait_vm<0>();
-      __syncthreads();  // K_{i+1}, V_i visible; every wave is done with tile i-1
+    issue_tile<D>((uint16_t*)smem, Kb + (size_t)b_cur * kBK * D, wave, lane);
+    if (PV) issue_tile<D>((uint16_t*)(smem + TILE), Vb + (size_t)b_cur * kBK * D, wave, lane);
+    for (int i = 0; i < count; ++i) {
       const bool has_next = i + 1 < count;
-      if (i + 2 < count)
-        issue_tile<D>((uint16_t*)(smem + kf * TILE), Kb + (size_t)blk(i + 2) * kBK * D, wave, lane);
-      if (PV && has_next)
-        issue_tile<D>((uint16_t*)(smem + (2 + vf) * TILE), Vb + (size_t)b_next * kBK * D, wave, lane);
+      const int b_nxt = has_next ? blk(i + 1) : 0;
+      wait_vm<PV ? G::LPT : 0>();  // K_i landed (V_i may still be in flight)
+      __syncthreads();
+      f32x16 s[4];
+      qk_tile<D>(s, lds, koff, qf);
+      __syncthreads();  // every wave is done with K_i
+      if (has_next) issue_tile<D>((uint16_t*)smem, Kb + (size_t)b_nxt * kBK * D, wave, lane);
+      if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
+      const float sc = tile_max<ENT>(s, scale_log2, st);
+      uint32_t pb[32];
       float lsum = 0.f, asum = 0.f;
-      if (has_next) {
-        // phase A: exps of S_i (VALU) while the matrix cores build S_{i+1}
-        // in the same registers, sub-tile by sub-tile
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
-#pragma unroll
-          for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < G::QK_STEPS; ++kk) qk_step<D>(s[kt], lds + kn * TILE, koff, qf, kt, kk);
-        }
-      } else {
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
+      for (int kt = 0; kt < 4; ++kt) {
+        tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
       }
       st.l += lsum;
       if (ENT) st.a += asum;
       if constexpr (PV) {
-        // phase B: O <- sc O + V_i P_i (matrix cores) while the VALU takes the
-        // max of S_{i+1}
-        if (__ballot(sc != 1.0f) != 0) {  // multiplying by exactly 1 changes nothing
+        if (has_next) wait_vm<G::LPT>();  // V_i landed (K_{i+1} may still be in flight)
+        else wait_vm<0>();
+        __syncthreads();
+        if (__ballot(sc != 1.0f) != 0) {
 #pragma unroll
           for (int dt = 0; dt < G::D_TILES; ++dt)
 #pragma unroll
@@ -367,27 +362,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-          for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], lds + (2 + vc) * TILE, voff, pb, ks, dt);
+          for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], lds + TILE, voff, pb, ks, dt);
+        sched_reads_ahead<8 * G::D_TILES, 2, 4>();
+        __syncthreads();  // every wave is done with V_i
+        if (has_next) issue_tile<D>((uint16_t*)(smem + TILE), Vb + (size_t)b_nxt * kBK * D, wave, lane);
       }
-      if (has_next) {
-        b_cur = b_next;
-        if (i + 2 < count) b_next = blk(i + 2);
-        if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
-        sc = tile_max<ENT>(s, scale_log2, st);
-      }
-    };
-
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    for (int i = 0;;) {
-      step(i, I1{}, I0{});  // K_{i+1} in K1, V_i in V0
-      if (++i >= count) break;
-      step(i, I0{}, I1{});  // K_{i+1} in K0, V_i in V1
-      if (++i >= count) break;
+      b_cur = b_nxt;
     }
   }
 
-  // ---- epilogue (cross-half sums first: every lane takes part in the exchange)
   const float l_tot = st.l + __shfl_xor(st.l, 32);
   const float a_tot = ENT ? st.a + __shfl_xor(st.a, 32) : 0.f;
   if (!qvalid) return;
@@ -399,7 +382,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
     for (int dt = 0; dt < G::D_TILES; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        // elements 4g..4g+3 hold d = 32dt + 8g + 4*half + {0,1,2,3}
         const int d0 = dt * 32 + 8 * g + 4 * half;
         uint2 w;
         w.x = pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv);
@@ -415,7 +397,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(
 
 template <int D, bool SPARSE, bool PV, bool ENT>
 void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT>), dim3(p.rows), dim3(kThreads), 0, s,
+  // the fused entropy + output variant needs more than the 256 VGPRs a wave
+  // gets at two workgroups per CU
+  constexpr int kOcc = (PV && ENT) ? 1 : 2;
+  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), 0, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
                      a.cnt, a.cols, a.order, p.N, p.n_pad, p.NB, p.rows,
                      (float)(1.4426950408889634 / std::sqrt((double)D)));
