@@ -95,6 +95,156 @@ def cpu_baseline(w, q_np, k_np, v_np, budget_s: float):
     }
 
 
+def density_sweep(tra, plan, w, q, k, v, dense_ms, targets, iters=3):
+    """Sparse attention at prescribed retained fractions.
+
+    Masks come from a UNIFORM token budget K_hat for every query (the paper's
+    "w/o Budget Mapping" ablation): a constant entropy ln(K_hat / tau) goes
+    through the same budget/radius and Alg. 1 mask kernels.  K_hat is searched
+    so the retained fraction lands nearest each target.  Q, K, V are the
+    workload's own."""
+    import math
+
+    import torch
+    B, Ha, N, d = q.shape
+    NB = plan.n_blocks
+    dev = q.device
+    H = torch.empty(B, Ha, N, dtype=torch.float32, device=dev)
+    rad = torch.empty(B, Ha, N, dtype=torch.int32, device=dev)
+    mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
+    cnt = torch.empty(B, Ha, NB, dtype=torch.int32, device=dev)
+    cols = torch.empty(B, Ha, NB, NB, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    nvec = torch.full((NB,), float(w.block), dtype=torch.float64, device=dev)
+    nvec[-1] = N - (NB - 1) * w.block
+    dense_flops = 4.0 * d * N * N * B * Ha
+
+    def build(khat):
+        H.fill_(math.log(khat / w.tau))   # ceil(tau * e^H) = khat, up to fp32 rounding of H
+        tra.tra_budget_radius(plan, H, None, rad)
+        tra.tra_build_block_mask(plan, rad, mask, cnt, cols, None)
+        m = mask.to(torch.float64)
+        fl = 4.0 * d * float(torch.einsum("bhuv,u,v->", m, nvec, nvec))
+        return fl / dense_flops, fl
+
+    rows = []
+    for target in targets:
+        lo, hi = 1, N
+        best = None
+        while lo <= hi:                      # retained fraction grows with K_hat
+            mid = (lo + hi) // 2
+            rho, fl = build(mid)
+            if best is None or abs(rho - target) < abs(best[1] - target):
+                best = (mid, rho, fl)
+            if rho < target:
+                lo = mid + 1
+            else:
+                hi = mid - 1
+        khat, rho, fl = best
+        build(khat)
+        h32 = float(np.float32(math.log(khat / w.tau)))
+        khat = int(min(max(math.ceil(w.tau * math.exp(h32)), 1), N))   # the budget actually used
+        tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(iters):
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+            b_.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b_))
+        ms = float(np.mean(ts))
+        rows.append({"target": target, "uniform_budget": khat, "retained_fraction": round(rho, 5),
+                     "sparse_ms": round(ms, 4), "tflops_executed": round(fl / (ms * 1e-3) / 1e12, 2),
+                     "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                     "speedup_vs_dense": round(dense_ms / ms, 4),
+                     "eta_proportionality": round(rho * dense_ms / ms, 4)})
+        log(f"density {target}: K_hat {khat} rho {rho:.4f} sparse {ms:.3f} ms")
+    return rows
+
+
+def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100):
+    """Warm-up reuse sequence: step 0 from the generator, later steps drift
+    q, k <- q, k + 0.02 N(0,1) (fp32 masters, re-rounded).  Every `refresh`
+    steps the fused entropy + dense output pass, budget/radius and mask are
+    recomputed (a refresh step); the other steps run sparse attention with the
+    cached lists (a reuse step).  Per-step times come from HIP events.  Mask
+    drift compares, untimed, each reused mask with a fresh one built from that
+    step's own entropy."""
+    import torch
+
+    import synth
+    feats = synth._features(w)
+    qs, ks, vs = [], [], []
+    for h in range(w.heads):
+        (q_, k_, v_), (qm, km) = synth.generate_head(w, 0, h, feats, masters=True)
+        qs.append(torch.from_numpy(qm))
+        ks.append(torch.from_numpy(km))
+        vs.append(torch.from_numpy(v_.view(np.int16)).view(torch.bfloat16))
+    q32 = torch.stack(qs)[None].cuda()
+    k32 = torch.stack(ks)[None].cuda()
+    v = torch.stack(vs)[None].cuda()
+    plan = tra.Plan(tra.Config.from_workload(w))
+    B, Ha, N, d = q32.shape
+    NB = plan.n_blocks
+    dev = q32.device
+    H = torch.empty(B, Ha, N, dtype=torch.float32, device=dev)
+    rad = torch.empty(B, Ha, N, dtype=torch.int32, device=dev)
+    mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
+    cnt = torch.empty(B, Ha, NB, dtype=torch.int32, device=dev)
+    cols = torch.empty(B, Ha, NB, NB, dtype=torch.int32, device=dev)
+    fmask = torch.empty_like(mask)
+    fcnt, fcols = torch.empty_like(cnt), torch.empty_like(cols)
+    o = torch.empty(B, Ha, N, d, dtype=torch.bfloat16, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + seed_offset)
+    refresh_ms, reuse_ms, drift = [], [], []
+    for t in range(steps):
+        if t > 0:
+            q32 += 0.02 * torch.randn(q32.shape, generator=gen, device=dev)
+            k32 += 0.02 * torch.randn(k32.shape, generator=gen, device=dev)
+        q, k = q32.to(torch.bfloat16), k32.to(torch.bfloat16)
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if t % refresh == 0:
+            a.record()
+            tra.tra_entropy(plan, q, k, v, o, H)
+            tra.tra_budget_radius(plan, H, None, rad)
+            tra.tra_build_block_mask(plan, rad, mask, cnt, cols, None)
+            b_.record()
+            torch.cuda.synchronize()
+            refresh_ms.append(a.elapsed_time(b_))
+        else:
+            a.record()
+            tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+            b_.record()
+            torch.cuda.synchronize()
+            reuse_ms.append(a.elapsed_time(b_))
+            tra.tra_entropy(plan, q, k, None, None, H)          # untimed fresh mask
+            tra.tra_budget_radius(plan, H, None, rad)
+            tra.tra_build_block_mask(plan, rad, fmask, fcnt, fcols, None)
+            m0, m1 = mask.bool(), fmask.bool()
+            inter = (m0 & m1).sum().item()
+            union = (m0 | m1).sum().item()
+            drift.append(((m0 ^ m1).float().mean().item(), 1.0 - inter / max(union, 1)))
+    dense_flops = 4.0 * d * N * N * B * Ha
+    nvec = torch.full((NB,), float(w.block), dtype=torch.float64, device=dev)
+    nvec[-1] = N - (NB - 1) * w.block
+    rho = float(torch.einsum("bhuv,u,v->", mask.to(torch.float64), nvec, nvec)) * 4.0 * d / dense_flops
+    total = sum(refresh_ms) + sum(reuse_ms)
+    return {
+        "workload": (f"{w.name}: {steps} steps, {w.heads} heads, head_dim {w.head_dim}, "
+                     f"{w.frames}x{w.height}x{w.width} = {N} tokens, refresh every {refresh}"),
+        "per_step_ms": round(total / steps, 4),
+        "refresh_step_ms": round(float(np.mean(refresh_ms)), 4),
+        "reuse_step_ms": round(float(np.mean(reuse_ms)), 4),
+        "retained_fraction_last_mask": round(rho, 5),
+        "mask_drift_hamming_mean": float(np.mean([x[0] for x in drift])),
+        "mask_drift_hamming_max": float(np.max([x[0] for x in drift])),
+        "mask_drift_jaccard_mean": float(np.mean([x[1] for x in drift])),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -106,6 +256,9 @@ def main():
     ap.add_argument("--dense-iters", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the density sweep and the warm-up reuse sequence")
+    ap.add_argument("--reuse-steps", type=int, default=50)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -259,6 +412,12 @@ def main():
             "traffic": None,
         },
     }
+    if not args.no_extras and w.dtype == "bf16":
+        log("density sweep at the paper's retained fractions (uniform budgets)")
+        out["density_sweep"] = density_sweep(tra, plan, w, q, k, v, dn, [0.09, 0.15, 0.19])
+        rw = synth.workload("reuse_480p")
+        log(f"warm-up reuse sequence ({args.reuse_steps} steps)")
+        out["reuse_sequence"] = reuse_driver(tra, rw, steps=args.reuse_steps)
     if not args.no_cpu:
         log(f"cpu baseline: oracle on a bounded sample (~{args.cpu_seconds:.0f} s)")
         out["cpu_baseline"] = cpu_baseline(w, q_np, k_np, v_np, args.cpu_seconds)
