@@ -35,6 +35,24 @@ def log(msg):
     sys.stderr.flush()
 
 
+def profiled_traffic():
+    """HBM-side bytes per sparse-attention launch from the committed counter
+    summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "counters_wan14b_720p.md")
+    src = os.path.join(ROOT, "paper_2608_02504_amd", "csrc", "attn_bf16.hip")
+    try:
+        text = open(path).read()
+        sha = re.search(r"kernel_source_sha256: ([0-9a-f]{64})", text).group(1)
+        val = int(re.search(r"sparse_traffic_bytes_per_launch: (\d+)", text).group(1))
+    except (OSError, AttributeError):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != sha:
+        return None
+    return val
+
+
 def executed_flops(mask: np.ndarray, N: int, b: int, d: int) -> float:
     """4 d sum over retained (u, v) of n_u n_v: QK^T and PV on valid pairs only."""
     nb = mask.shape[-1]
@@ -259,7 +277,18 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the density sweep and the warm-up reuse sequence")
     ap.add_argument("--reuse-steps", type=int, default=50)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": 1 << 30, "copies": 3}))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only; this build has no multi-GPU path "
@@ -409,7 +438,8 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": profiled_traffic() if args.workload == "wan14b_720p" else None,
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
         },
     }
     if not args.no_extras and w.dtype == "bf16":
