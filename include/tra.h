@@ -44,10 +44,15 @@
  * Every compute call is asynchronous on `stream` (a hipStream_t passed as
  * void*, NULL = the null stream), checks its arguments before launching, and
  * returns a status.  The caller owns every tensor buffer and keeps it alive
- * until the stream has drained.  The plan owns only its small device tables
- * and a sort workspace; it is immutable after creation, and calls that share a
- * plan must not overlap in time on different streams when they use the
- * sort workspace (tra_build_block_mask with a non-NULL order).  No C++
+ * until the stream has drained.  The plan owns its small device tables, a
+ * sort workspace and, for bf16 plans, a key/value workspace of
+ * 2 x batch x heads x NB x 128 x head_dim x 2 bytes into which every
+ * attention call (tra_entropy, tra_sparse_attention, tra_dense_attention)
+ * first rewrites K and V in tile-major order (V transposed per block).  Calls
+ * that share a plan must therefore not overlap in time on different streams
+ * when they use a workspace (those three calls on bf16 plans, and
+ * tra_build_block_mask with a non-NULL order); calls on one stream are ordered
+ * and safe.  Otherwise the plan is immutable after creation.  No C++
  * exception crosses this ABI.  On failure, tra_last_error() returns a message
  * for the calling thread.
  */
@@ -154,8 +159,9 @@ tra_status tra_budget_radius(tra_plan plan, const float* entropy, int32_t* budge
  * covers key j iff (x_i-x_j)^2 + (y_i-y_j)^2 <= thr[n_i][|f_i - f_j|]
  * (Eq. 15); radius values outside [0, n_cap] other than TRA_RADIUS_FULL are
  * clamped (negative -> 0, larger -> FULL).  The rule comes from the plan.
- * mask: uint8 output or NULL; cnt, cols: int32 outputs; order: int32 output or
- * NULL (uses the plan's sort workspace). */
+ * mask: uint8 output or NULL; cnt, cols: int32 outputs; order: int32 output
+ * (the heaviest-first row order, sorted in the plan's sort workspace) or NULL
+ * (not computed). */
 tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t* mask,
                                 int32_t* cnt, int32_t* cols, int32_t* order,
                                 void* stream);

@@ -5,30 +5,32 @@
 // Layout pre-pass
 //   K and V are first gathered into tile-major order (Sec. 3.3: tokens of a
 //   spatial tile become contiguous) in the plan's workspace, one 128-token key
-//   block = one contiguous 32 KB tile, rows past N zero-filled.  The attention
-//   loop then addresses tiles affinely.  Q is gathered and O scattered through
-//   the same permutation inside the kernel, so callers keep raster order.
+//   block = one contiguous tile, rows past N zero-filled: K as 128 rows x D,
+//   V transposed (D rows x 128 keys), so that both matrix operands are read
+//   from LDS with plain 16-byte reads.  The attention loop then addresses
+//   tiles affinely.  Q is gathered and O scattered through the same
+//   permutation inside the kernel, so callers keep raster order.
 //
 // Work decomposition
 //   One workgroup (4 waves, 256 threads) per query-block row r = (b, h, u):
 //   128 queries, wave w owning queries [32w, 32w + 32).  It walks the key
 //   blocks of its row (all NB for dense; cols[r][0..cnt[r]) for sparse), 128
-//   keys per tile.  Two workgroups share a CU (64 KB of LDS each), so every
-//   SIMD runs one workgroup's matrix phase while the other is in its softmax.
+//   keys per tile.  Two workgroups share a CU (64 KB of LDS each), so a SIMD
+//   can run one workgroup's matrix phase while the other is in its softmax.
 //
 // Per tile (split barriers)
-//   K and V go from HBM straight into LDS (global_load_lds_dwordx4, no register
-//   staging), 16-byte chunks XOR-swizzled per row so K reads and transposed V
-//   reads hit every bank once.  The next K tile streams in during softmax + PV,
-//   the next V tile during QK^T + softmax.  Scheduling hints keep several LDS
-//   operand reads in flight ahead of the MFMAs.
+//   K and V^T go from HBM straight into LDS (global_load_lds_dwordx4 from a
+//   scalar tile base, no register staging), 16-byte chunks XOR-swizzled per
+//   row so that operand reads hit every bank once.  The next K tile streams in
+//   during softmax + PV, the next V^T tile during QK^T + softmax.  Scheduling
+//   hints keep four LDS operand reads in flight ahead of the MFMAs.
 //
 // Matrix work (v_mfma_f32_32x32x16_bf16, fp32 accumulation)
 //   S^T = K Q^T: keys are the M side and the wave's 32 queries the N side, so a
 //   lane holds 64 scores of ONE query (row max / row sum are in-lane plus one
-//   exchange between lane halves).  The bf16 probabilities stay in registers
-//   as the B operand of O^T += V^T P^T; the V^T operand comes from LDS through
-//   ds_read_b64_tr_b16, which transposes 16-bit elements across lanes.
+//   cross-half lane swap).  The bf16 probabilities stay in registers as the B
+//   operand of O^T += V^T P^T; K rows are loaded in an order that leaves every
+//   lane half holding 8 consecutive keys, the k-slice a V^T row chunk covers.
 //
 // Softmax and entropy (Alg. 2 with the running sum kept relative to the max)
 //   x = s alpha log2(e) - m,  w = 2^x,  l = sum w,  a = sum w x.
@@ -36,7 +38,6 @@
 //   H = ln(l) - ln(2) a / l  (nats)  == log Z - sum_j p_j s_j (App. C.2).
 //   Each lane keeps l and a over its own keys; the halves are added at the end.
 #include <cmath>
-#include <type_traits>
 
 #include "tra_internal.h"
 
@@ -45,11 +46,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kBQ = 128;       // queries per workgroup (= block size)
 constexpr int kBK = 128;       // keys per tile (= block size)
@@ -61,11 +59,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-// XOR swizzle of the 16-byte chunks of LDS row `row` (one key).  Row length is
-// D*2 bytes = CH chunks.  Requirements: (a) 16 consecutive rows read at one
-// logical chunk land in distinct banks (QK^T operand reads); (b) 4 aligned
-// consecutive rows read at 4 aligned consecutive chunks land in distinct
-// banks (transposed V reads).
+// XOR swizzle of the 16-byte chunks of LDS row `row` (one K row of D*2 bytes =
+// CH chunks, or one V^T row of 128 keys = 16 chunks): 16 consecutive rows read
+// at one logical chunk, which is what the 16 lanes of one LDS cycle of an
+// operand read ask for, land in 16 distinct bank groups.
 template <int CH>
 __device__ __forceinline__ int swz(int row) {
   if constexpr (CH == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
@@ -79,55 +76,140 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations,
+// then s_barrier.  __syncthreads() would also drain every outstanding global
+// load (its release fence), which would stall on the tile loads that are
+// meant to stay in flight across the barrier; tile readiness is instead
+// established with explicit vmcnt waits before the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // ------------------------------------------------------------ layout pre-pass
-// dst[bh][p][:] = src[bh][perm[p]][:] for p < N, 0 for N <= p < n_pad.
-__global__ __launch_bounds__(256) void gather_kv_kernel(const uint4* __restrict__ k,
-                                                        const uint4* __restrict__ v,
-                                                        uint4* __restrict__ kt, uint4* __restrict__ vt,
-                                                        const int32_t* __restrict__ perm, int N,
-                                                        int n_pad, int ch, long long total) {
+// kt[bh][p][:] = k[bh][perm[p]][:] for p < N, 0 for N <= p < n_pad.
+__global__ __launch_bounds__(256) void gather_k_kernel(const uint4* __restrict__ k,
+                                                       uint4* __restrict__ kt,
+                                                       const int32_t* __restrict__ perm, int N,
+                                                       int n_pad, int ch, long long total) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= total) return;
   const long long per_head = (long long)n_pad * ch;
   const long long bh = idx / per_head;
   const long long rem = idx - bh * per_head;
   const int p = (int)(rem / ch), c = (int)(rem - (long long)p * ch);
-  uint4 zk = make_uint4(0, 0, 0, 0), zv = zk;
-  if (p < N) {
-    const long long s = (bh * N + perm[p]) * ch + c;
-    zk = k[s];
-    if (v) zv = v[s];
+  kt[idx] = p < N ? k[(bh * N + perm[p]) * ch + c] : make_uint4(0, 0, 0, 0);
+}
+
+// V transposed per key block, tile-major: for tile-major position p = 128 b + j,
+// vt[bh][b][d][j] = v[bh][perm[p]][d] (0 for N <= p < n_pad), so key block b of a
+// head is one contiguous D x 128 tile with the key index fastest.  One
+// workgroup per 64 tokens of one head, through LDS.
+template <int D>
+__global__ __launch_bounds__(256) void gather_vt_kernel(const uint16_t* __restrict__ v,
+                                                        uint16_t* __restrict__ vt,
+                                                        const int32_t* __restrict__ perm, int N,
+                                                        int n_pad) {
+  constexpr int TOK = 64, CH = D / 8, LS = D + 2;
+  __shared__ uint16_t tile[TOK * LS];
+  const int bh = blockIdx.y, p0 = blockIdx.x * TOK, t = threadIdx.x;
+  for (int i = t; i < TOK * CH; i += 256) {
+    const int j = i / CH, c = i - j * CH;
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (p0 + j < N) x = *(const uint4*)(v + ((size_t)bh * N + perm[p0 + j]) * D + c * 8);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tile[j * LS + c * 8 + 2 * e] = (uint16_t)(w[e] & 0xFFFFu);
+      tile[j * LS + c * 8 + 2 * e + 1] = (uint16_t)(w[e] >> 16);
+    }
   }
-  kt[idx] = zk;
-  if (v) vt[idx] = zv;
+  __syncthreads();
+  for (int i = t; i < D * (TOK / 8); i += 256) {
+    const int d = i / (TOK / 8), tc = i - d * (TOK / 8);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)tile[(tc * 8 + 2 * e) * LS + d] | ((uint32_t)tile[(tc * 8 + 2 * e + 1) * LS + d] << 16);
+    const int p = p0 + tc * 8;
+    *(uint4*)(vt + (size_t)bh * n_pad * D + ((size_t)(p / kBK) * D + d) * kBK + p % kBK) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
 }
 
 // ------------------------------------------------------------ attention
 template <int D>
 struct Geo {
   static constexpr int CH = D / 8;                 // 16-byte chunks per row
-  static constexpr int LPT = kBK * CH / kThreads;  // direct loads per thread per tile
-  static constexpr int RPI = 64 / CH;              // rows covered by one wave-wide load
   static constexpr int QK_STEPS = D / 16;
   static constexpr int D_TILES = D / 32;
 };
 
-// Direct HBM -> LDS copy of one contiguous tile (kBK rows x D): load n of this
-// thread fills LDS slots [(4n + wave) * 64, +64), i.e. row (4n + wave) * RPI +
-// lane / CH, physical chunk lane % CH, which holds logical chunk
-// (lane % CH) ^ swz(row).
+// One 16-byte HBM -> LDS copy per lane (global_load_lds_dwordx4 with a scalar
+// base): lane i reads sbase + voff_i and its 16 bytes land at LDS address
+// lds_base + 16 i.  Issued as inline assembly so the compiler does not track
+// it: its conservative tracking of LDS-writing loads would wait for every tile
+// in flight before any LDS read.  Completion is established by the explicit
+// vmcnt waits before the barriers that publish a tile, so the loads stay in
+// flight across unrelated LDS work.  Nothing else in these kernels uses m0.
+// The LDS address is lds_base + LDS_STEP, formed in m0 by the same statement
+// so that no per-step copy of it is kept live.
+template <int LDS_STEP>
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_base), "i"(LDS_STEP)
+               : "memory", "m0", "scc");
+}
+
+// A tile (K: 128 rows x D; V^T: D rows x 128 keys; 32 KB or 16 KB, contiguous
+// in HBM) is copied by the 4 waves in 4 KB steps: step n of wave w fills LDS
+// bytes [4096 n + 1024 w, +1024) from HBM bytes 4096 n + tile_lane_off.  A
+// 4 KB step spans 16 K rows (D = 128) or 32 (D = 64), or 16 V^T rows, so row
+// mod 16 and with it the swizzle is the same in every step: the per-lane
+// offset is fixed and only the scalar base moves.
 template <int D>
-__device__ __forceinline__ void issue_tile(uint16_t* lds, const uint16_t* tile, int wave, int lane) {
-  using G = Geo<D>;
-  const int lrow0 = wave * G::RPI + lane / G::CH;
-  const int lphys = lane % G::CH;
-#pragma unroll
-  for (int n = 0; n < G::LPT; ++n) {
-    const int row = n * 4 * G::RPI + lrow0;
-    const int c = lphys ^ swz<G::CH>(row);
-    __builtin_amdgcn_global_load_lds((const void*)(tile + row * D + c * 8),
-                                     (lds_void*)(lds + (n * 4 + wave) * 64 * 8), 16, 0, 0);
+struct TileCopy {
+  static constexpr int STEPS = kBK * D * 2 / 4096;
+};
+
+// Lane offset within a 4 KB step of a K tile: row wave * RPI + lane / CH,
+// physical chunk lane % CH, which holds logical chunk (lane % CH) ^ swz(row).
+template <int D>
+__device__ __forceinline__ uint32_t k_lane_off(int wave, int lane) {
+  constexpr int CH = D / 8, RPI = 64 / CH;
+  const int row = wave * RPI + lane / CH;
+  return row * D * 2 + (((lane % CH) ^ swz<CH>(row)) << 4);
+}
+
+// Lane offset within a 4 KB step of a V^T tile (rows of 128 keys = 16 chunks):
+// row wave * 4 + lane / 16, physical chunk lane % 16.
+__device__ __forceinline__ uint32_t vt_lane_off(int wave, int lane) {
+  const int row = wave * 4 + lane / 16;
+  return row * kBK * 2 + (((lane % 16) ^ swz<16>(row)) << 4);
+}
+
+template <int N>
+__device__ __forceinline__ void issue_steps(uint32_t lds_wave, const uint8_t* tile, uint32_t lane_off) {
+  if constexpr (N > 0) {
+    issue_steps<N - 1>(lds_wave, tile, lane_off);
+    dma16<(N - 1) * 4096>(tile + (N - 1) * 4096, lane_off, lds_wave);
   }
+}
+
+template <int D>
+__device__ __forceinline__ void issue_tile(uint32_t lds_wave, const uint8_t* tile, uint32_t lane_off) {
+  issue_steps<TileCopy<D>::STEPS>(lds_wave, tile, lane_off);
+}
+
+// max / sum of a value over the two lane halves (lanes l and l ^ 32), with
+// one cross-half swap instead of an LDS round trip
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
@@ -136,11 +218,25 @@ __device__ __forceinline__ bf16x8 lds_read16(const lds_u8* base, uint32_t off) {
   return __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) uint4*)(base + off));
 }
 
-// One MFMA step of S^T = K Q^T for sub-tile kt: keys 32kt + (lane % 32).
+// Hides a value from the optimiser, so that offsets derived from it are
+// recomputed next to their use instead of being hoisted out of the tile loop
+// and kept live in registers.
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// LDS byte offset of logical 16-byte chunk 2k + h of a row whose chunks are
+// XOR-swizzled by sw: (2k + h) ^ sw == 2k ^ (h ^ sw), so with
+// base = row_bytes + ((h ^ sw) << 4) the offset is base ^ (k << 5): one XOR per
+// read (the row bytes are a multiple of 128, above the chunk bits).
+__device__ __forceinline__ uint32_t chunk_off(uint32_t base, int k) { return base ^ (uint32_t)(k << 5); }
+
+// One MFMA step of S^T = K Q^T for sub-tile kt and k-step kk.
 template <int D>
-__device__ __forceinline__ void qk_step(f32x16& s, const lds_u8* kbuf, const uint32_t (&koff)[Geo<D>::QK_STEPS],
+__device__ __forceinline__ void qk_step(f32x16& s, const lds_u8* __restrict__ kbuf, uint32_t koff_kk,
                                         const bf16x8 (&qf)[Geo<D>::QK_STEPS], int kt, int kk) {
-  const bf16x8 ka = lds_read16(kbuf, koff[kk] + kt * 32 * D * 2);
+  const bf16x8 ka = lds_read16(kbuf, koff_kk + kt * 32 * D * 2);
   s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s, 0, 0, 0);
 }
 
@@ -162,31 +258,38 @@ __device__ __forceinline__ void sched_reads_ahead() {
 }
 
 template <int D>
-__device__ __forceinline__ void qk_tile(f32x16 (&s)[4], const lds_u8* kbuf,
-                                        const uint32_t (&koff)[Geo<D>::QK_STEPS],
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[4], const lds_u8* __restrict__ kbuf, uint32_t kbase,
                                         const bf16x8 (&qf)[Geo<D>::QK_STEPS]) {
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
+  kbase = opaque(kbase);
   // k-step outer, sub-tile inner: four independent accumulation chains
 #pragma unroll
-  for (int kk = 0; kk < Geo<D>::QK_STEPS; ++kk)
+  for (int kk = 0; kk < Geo<D>::QK_STEPS; ++kk) {
+    const uint32_t off = chunk_off(kbase, kk);
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) qk_step<D>(s[kt], kbuf, koff, qf, kt, kk);
+    for (int kt = 0; kt < 4; ++kt) qk_step<D>(s[kt], kbuf, off, qf, kt, kk);
+  }
   sched_reads_ahead<4 * Geo<D>::QK_STEPS, 1, 4>();
 }
 
 // Keys past the end of a ragged last block get a large finite negative score:
 // their weight 2^x underflows to 0 and w * x stays 0 (not 0 * inf).
-// Output element e of sub-tile kt is key 32kt + 8(e/4) + 4*half + e%4.
+// Output element e of sub-tile kt is key 32kt + 16(e/8) + 8*half + e%8 (the
+// K rows are loaded in that order: krow in the kernel).  The select is done with
+// integer arithmetic (sign of key - nv as a bit mask) so that no per-element
+// lane mask is materialised in scalar registers.
 __device__ __forceinline__ void mask_tail(f32x16 (&s)[4], int nv, int half) {
+  const int base = 8 * half - nv;
+  const uint32_t neg = __float_as_uint(-1.0e30f);
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int key = kt * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-      if (key >= nv) s[kt][e] = -1.0e30f;
+      const uint32_t keep = (uint32_t)((kt * 32 + 16 * (e >> 3) + (e & 7) + base) >> 31);
+      s[kt][e] = __uint_as_float(((__float_as_uint(s[kt][e]) & keep) | (neg & ~keep)));
     }
 }
 
@@ -203,7 +306,7 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  mx = max_halves(mx);
   const float m_new = fmaxf(st.m, mx * scale_log2);
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
@@ -229,33 +332,19 @@ __device__ __forceinline__ void tile_exp(const f32x16& s, float scale_log2, floa
   }
 }
 
-// O^T += V^T P^T.  k-step ks covers keys [16ks, 16ks+16); in lane half h the B
-// operand (sub-tile ks/2, elements 8(ks%2)..+7) holds keys 16ks + 4h + {0..3}
-// and 16ks + 8 + 4h + {0..3}.  ds_read_b64_tr_b16 gives output lane i (of a
-// 16-lane group) element (i%4) of the 8-byte rows addressed by lanes i/4 + 4k,
-// k = 0..3: so lane j of group g addresses key 16ks + 4h + j/4 (+8 for the
-// second read) at d = 32dt + 16(g%2) + 4(j%4), and lane i receives
-// d = 32dt + (lane % 32) with keys 16ks + 4h + {0..3} (+8).
+// O^T += V^T P^T.  k-step ks covers keys [16ks, 16ks+16); in lane half h the
+// B operand (sub-tile ks/2, elements 8(ks%2)..+7) holds the 8 consecutive keys
+// 16ks + 8h + {0..7}, and the A operand row d = 32dt + (lane % 32) of V^T is the
+// 16-byte chunk (2ks + h) of that row in LDS.
 template <int D>
-__device__ __forceinline__ void pv_step(f32x16& oacc, const lds_u8* vbuf, const uint32_t (&voff)[2][Geo<D>::D_TILES],
+__device__ __forceinline__ void pv_step(f32x16& oacc, const lds_u8* __restrict__ vbuf, uint32_t voff_ks,
                                         const uint32_t (&pb)[32], int ks, int dt) {
   const int kt = ks >> 1, eb = (ks & 1) * 4;
   const uint4 bw = make_uint4(pb[kt * 8 + eb], pb[kt * 8 + eb + 1], pb[kt * 8 + eb + 2], pb[kt * 8 + eb + 3]);
-  const uint32_t o0 = voff[0][dt] + ks * 16 * D * 2, o1 = voff[1][dt] + ks * 16 * D * 2;
-  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbuf + o0));
-  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbuf + o1));
-  const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-  const uint4 va4 = make_uint4(l2.x, l2.y, h2.x, h2.y);
-  oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va4),
-                                                 __builtin_bit_cast(bf16x8, bw), oacc, 0, 0, 0);
+  const bf16x8 va = lds_read16(vbuf, voff_ks + dt * 32 * kBK * 2);
+  oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, __builtin_bit_cast(bf16x8, bw), oacc, 0, 0, 0);
 }
 
-// Main attention kernel.  One workgroup per query-block row, two workgroups per
-// CU (64 KB of LDS each: one K and one V tile).  Split barriers let the next
-// K tile stream in during softmax + PV and the next V tile during QK^T +
-// softmax; each SIMD interleaves one workgroup's matrix phase with the other's
-// vector phase.  OCC is the workgroups-per-CU bound the registers are sized
-// for (the fused entropy + output variant needs one per CU to avoid spills).
 template <int D, bool SPARSE, bool PV, bool ENT, int OCC>
 __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
@@ -265,8 +354,12 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     int rows, float scale_log2) {
   using G = Geo<D>;
   constexpr int TILE = kBK * D * 2;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[(PV ? 2 : 1) * TILE];  // [K][V]
-  lds_u8* lds = (lds_u8*)smem;
+  __shared__ __attribute__((aligned(1024))) uint8_t smemK[TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t smemV[PV ? TILE : 16];
+  // the row's key-block list (dynamic LDS, NB entries for the sparse variant),
+  // read once so that the tile loop issues no global loads of its own (a wait
+  // for one would also drain the tiles in flight)
+  extern __shared__ int32_t smemCols[];
 
   int r = blockIdx.x;
   if (SPARSE && order) {
@@ -274,11 +367,17 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     if (r < 0 || r >= rows) return;
   }
   const int bh = r / NB, u = r - bh * NB;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int col = lane & 31, half = lane >> 5;
   const size_t head_off = (size_t)bh * N * D;
-  const uint16_t* Kb = ktile + (size_t)bh * n_pad * D;
-  const uint16_t* Vb = vtile + (size_t)bh * n_pad * D;
+  constexpr size_t kTileBytes = (size_t)kBK * D * 2;
+  const uint8_t* Kb = (const uint8_t*)(ktile + (size_t)bh * n_pad * D);
+  const uint8_t* Vb = (const uint8_t*)(vtile + (size_t)bh * n_pad * D);  // V^T tiles of this head
+  const uint32_t k_lds = (uint32_t)(uintptr_t)smemK + wave * 1024;
+  const uint32_t v_lds = (uint32_t)(uintptr_t)smemV + wave * 1024;
+  const uint32_t k_off = k_lane_off<D>(wave, lane);
+  const uint32_t v_off = vt_lane_off(wave, lane);
 
   const int qpos = u * kBQ + wave * 32 + col;
   const bool qvalid = qpos < N;
@@ -292,32 +391,43 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
       qf[kk] = __builtin_bit_cast(bf16x8, x);
     }
   }
-  uint32_t koff[G::QK_STEPS];
-  {
-    const int sw = swz<G::CH>(col);
-#pragma unroll
-    for (int kk = 0; kk < G::QK_STEPS; ++kk) koff[kk] = col * D * 2 + (((2 * kk + half) ^ sw) << 4);
+  const int count = SPARSE ? min(max(cnt[r], 0), NB) : NB;
+  if constexpr (SPARSE) {
+    const int32_t* colp = cols + (size_t)r * NB;
+    for (int j = t; j < count; j += kThreads) smemCols[j] = colp[j];
   }
-  uint32_t voff[2][G::D_TILES];
-  {
-    const int grp = lane >> 4, j = lane & 15;
-    const int kj = 4 * half + (j >> 2);
-    const int dq = 16 * (grp & 1) + 4 * (j & 3);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int key = kj + 8 * h;
-      const int sw = swz<G::CH>(key);
-#pragma unroll
-      for (int dt = 0; dt < G::D_TILES; ++dt) {
-        const int d = 32 * dt + dq;
-        voff[h][dt] = key * D * 2 + ((((d >> 3) ^ sw) << 3) + (d & 7)) * 2;
+  // retire the Q and list loads before any tile load is in flight, so that no
+  // compiler wait for them lands inside the tile loop (it would also drain the
+  // tiles), and publish the list
+  wait_vm<0>();
+  lds_barrier();
+  // QK^T operand rows: lane (row m = lane % 32) loads key row krow(m)
+  // of each 32-key sub-tile, chosen so that lane half h ends up holding the 8
+  // consecutive keys 8h..8h+7 (and 16+8h..) of the sub-tile: output row
+  // R = 8(e/4) + 4h + e%4 must be key 16(e/8) + 8h + e%8, i.e. rows 4..7 and
+  // 8..11 of every 16 swap places.
+  const int krow = (col & ~15) | ((col & 15) ^ (((col >> 2) & 3) == 1 || ((col >> 2) & 3) == 2 ? 12 : 0));
+  const uint32_t kbase = krow * D * 2 + ((half ^ swz<G::CH>(krow)) << 4);
+  // V^T operand: row d = 32dt + (lane % 32) (dt as an immediate), chunk 2ks + h
+  const uint32_t vbase = col * kBK * 2 + ((half ^ swz<16>(col)) << 4);
+
+  // Next list position at or after i holding a valid key block, or count;
+  // entries outside [0, NB) are skipped.  *b receives the block id.
+  auto next_valid = [&](int i, int* b) -> int {
+    if (!SPARSE) {
+      *b = i;
+      return i;
+    }
+    for (; i < count; ++i) {
+      const int c = smemCols[i];
+      if (c >= 0 && c < NB) {
+        *b = c;
+        return i;
       }
     }
-  }
-
-  const int count = SPARSE ? min(max(cnt[r], 0), NB) : NB;
-  const int32_t* colp = SPARSE ? cols + (size_t)r * NB : nullptr;
-  auto blk = [&](int i) -> int { return SPARSE ? min(max(colp[i], 0), NB - 1) : i; };
+    *b = 0;
+    return count;
+  };
 
   f32x16 oacc[PV ? G::D_TILES : 1];
 #pragma unroll
@@ -326,19 +436,21 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
   RowState st{-INFINITY, 0.f, 0.f};
 
-  if (count > 0) {
-    int b_cur = blk(0);
-    issue_tile<D>((uint16_t*)smem, Kb + (size_t)b_cur * kBK * D, wave, lane);
-    if (PV) issue_tile<D>((uint16_t*)(smem + TILE), Vb + (size_t)b_cur * kBK * D, wave, lane);
-    for (int i = 0; i < count; ++i) {
-      const bool has_next = i + 1 < count;
-      const int b_nxt = has_next ? blk(i + 1) : 0;
-      wait_vm<PV ? G::LPT : 0>();  // K_i landed (V_i may still be in flight)
-      __syncthreads();
+  int b_cur;
+  int i = next_valid(0, &b_cur);
+  if (i < count) {
+    issue_tile<D>(k_lds, Kb + b_cur * kTileBytes, k_off);
+    if (PV) issue_tile<D>(v_lds, Vb + b_cur * kTileBytes, v_off);
+    for (;;) {
+      int b_nxt;
+      const int i_nxt = next_valid(i + 1, &b_nxt);
+      const bool has_next = i_nxt < count;
+      wait_vm<PV ? TileCopy<D>::STEPS : 0>();  // K_i landed (V_i may still be in flight)
+      lds_barrier();
       f32x16 s[4];
-      qk_tile<D>(s, lds, koff, qf);
-      __syncthreads();  // every wave is done with K_i
-      if (has_next) issue_tile<D>((uint16_t*)smem, Kb + (size_t)b_nxt * kBK * D, wave, lane);
+      qk_tile<D>(s, (const lds_u8*)smemK, kbase, qf);
+      lds_barrier();  // every wave is done with K_i
+      if (has_next) issue_tile<D>(k_lds, Kb + b_nxt * kTileBytes, k_off);
       if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
       const float sc = tile_max<ENT>(s, scale_log2, st);
       uint32_t pb[32];
@@ -350,29 +462,34 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
       st.l += lsum;
       if (ENT) st.a += asum;
       if constexpr (PV) {
-        if (has_next) wait_vm<G::LPT>();  // V_i landed (K_{i+1} may still be in flight)
+        if (has_next) wait_vm<TileCopy<D>::STEPS>();  // V_i landed (K_{i+1} may still be in flight)
         else wait_vm<0>();
-        __syncthreads();
+        lds_barrier();
         if (__ballot(sc != 1.0f) != 0) {
 #pragma unroll
           for (int dt = 0; dt < G::D_TILES; ++dt)
 #pragma unroll
             for (int e = 0; e < 16; ++e) oacc[dt][e] *= sc;
         }
+        const uint32_t vb0 = opaque(vbase);
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
+        for (int ks = 0; ks < 8; ++ks) {
+          const uint32_t off = chunk_off(vb0, ks);
 #pragma unroll
-          for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], lds + TILE, voff, pb, ks, dt);
-        sched_reads_ahead<8 * G::D_TILES, 2, 4>();
-        __syncthreads();  // every wave is done with V_i
-        if (has_next) issue_tile<D>((uint16_t*)(smem + TILE), Vb + (size_t)b_nxt * kBK * D, wave, lane);
+          for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], (const lds_u8*)smemV, off, pb, ks, dt);
+        }
+        sched_reads_ahead<8 * G::D_TILES, 1, 4>();
+        lds_barrier();  // every wave is done with V_i
+        if (has_next) issue_tile<D>(v_lds, Vb + b_nxt * kTileBytes, v_off);
       }
+      if (!has_next) break;
+      i = i_nxt;
       b_cur = b_nxt;
     }
   }
 
-  const float l_tot = st.l + __shfl_xor(st.l, 32);
-  const float a_tot = ENT ? st.a + __shfl_xor(st.a, 32) : 0.f;
+  const float l_tot = sum_halves(st.l);
+  const float a_tot = ENT ? sum_halves(st.a) : 0.f;
   if (!qvalid) return;
   const size_t tok = (size_t)bh * N + qrow;
   if (PV) {
@@ -397,24 +514,31 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
 
 template <int D, bool SPARSE, bool PV, bool ENT>
 void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   // the fused entropy + output variant needs more than the 256 VGPRs a wave
   // gets at two workgroups per CU
   constexpr int kOcc = (PV && ENT) ? 1 : 2;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), 0, s,
+  const size_t list_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
+  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), list_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
-                     a.cnt, a.cols, a.order, p.N, p.n_pad, p.NB, p.rows,
-                     (float)(1.4426950408889634 / std::sqrt((double)D)));
+                     a.cnt, a.cols, a.order, p.N, p.n_pad, p.NB, p.rows, scale_log2);
 }
 
 template <int D>
 hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const int ch = D / 8;
-  const long long total = (long long)p.cfg.batch * p.cfg.heads * p.n_pad * ch;
-  hipLaunchKernelGGL(gather_kv_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     (const uint4*)a.k, (const uint4*)a.v, (uint4*)p.d_kt, (uint4*)p.d_vt, p.d_perm,
-                     p.N, p.n_pad, ch, total);
+  const int bhs = p.cfg.batch * p.cfg.heads;
+  const long long total = (long long)bhs * p.n_pad * ch;
+  hipLaunchKernelGGL(gather_k_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                     (const uint4*)a.k, (uint4*)p.d_kt, p.d_perm, p.N, p.n_pad, ch, total);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.v) {
+    hipLaunchKernelGGL((gather_vt_kernel<D>), dim3(p.n_pad / 64, bhs), dim3(256), 0, s,
+                       (const uint16_t*)a.v, p.d_vt, p.d_perm, p.N, p.n_pad);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (a.sparse) launch_variant<D, true, true, false>(p, a, s);
   else if (a.entropy && a.o) launch_variant<D, false, true, true>(p, a, s);
   else if (a.entropy) launch_variant<D, false, false, true>(p, a, s);

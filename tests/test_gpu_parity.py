@@ -132,6 +132,45 @@ def test_zero_radius_is_block_diagonal(name):
             assert np.abs(O_gpu[idx] - want).max() <= tol
 
 
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny"])
+def test_out_of_range_column_ids_are_skipped(name):
+    """Key-block ids outside [0, NB) in a list are skipped: padding every list
+    with -1 and NB entries (between and around the valid ids) leaves o and lse
+    bitwise equal to the call with the clean list."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    w = SMALL[name]
+    run = Run(w)
+    NB = run.plan.n_blocks
+    cnt, cols = run.cnt.cpu().numpy(), run.cols.cpu().numpy()
+    cnt2 = np.zeros_like(cnt)
+    cols2 = np.full_like(cols, -1)
+    rng = np.random.default_rng(7)
+    padded = 0
+    for idx in np.ndindex(cnt.shape):
+        valid = cols[idx][:cnt[idx]].tolist()
+        out = []
+        for c in valid:
+            out += [-1, NB][:rng.integers(0, 3)]  # 0, 1 or 2 invalid ids first
+            out.append(c)
+        out = (out + [NB, -5])[:NB]  # a list holds at most NB entries
+        kept = [c for c in out if 0 <= c < NB]
+        padded += len(out) - len(kept)
+        cnt2[idx], cols2[idx][:len(out)] = len(out), out
+        cnt[idx], cols[idx][:len(kept)] = len(kept), kept
+    assert padded > 0
+    dev = run.q.device
+    ref_o, ref_l = torch.empty_like(run.O_sp), torch.empty_like(run.lse_sp)
+    got_o, got_l = torch.empty_like(run.O_sp), torch.empty_like(run.lse_sp)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    tra.tra_sparse_attention(run.plan, run.q, run.k, run.v, t(cnt), t(cols), None, ref_o, ref_l)
+    tra.tra_sparse_attention(run.plan, run.q, run.k, run.v, t(cnt2), t(cols2), None, got_o, got_l)
+    torch.cuda.synchronize()
+    assert torch.equal(got_o, ref_o)
+    assert torch.equal(got_l, ref_l)
+
+
 def test_determinism_bitwise():
     _gpu()
     import torch
