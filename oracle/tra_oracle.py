@@ -24,9 +24,11 @@ the design notes; each function below names the passage it follows.
 from __future__ import annotations
 
 import math
+from statistics import NormalDist
 
 import numpy as np
 import torch
+from scipy.special import erfc
 
 RADIUS_FULL = 2 ** 31 - 1
 
@@ -37,7 +39,9 @@ __all__ = [
     "within_radius", "grid_count_bruteforce", "disk_count_table", "grid_count",
     "select_radius", "select_radius_linear", "token_mask_rows",
     "block_mask_rows", "masked_attention_rows", "retained_fraction",
-    "top_tau_support", "analytic_radius",
+    "top_tau_support", "analytic_radius", "token_budget_lognormal",
+    "lognormal_top_mass", "normal_quantile", "normal_tail", "threshold_table_1d",
+    "within_radius_1d", "joint_order",
 ]
 
 
@@ -65,6 +69,14 @@ def tile_major_order(F: int, H: int, W: int, tile_h: int, tile_w: int) -> np.nda
                     frame.append(x * W + y)
     frame = np.asarray(frame, dtype=np.int64)
     return np.concatenate([f * H * W + frame for f in range(F)])
+
+
+def joint_order(perm_video, text_tokens: int) -> np.ndarray:
+    """Sequence order of joint text-video attention (Sec. 3.2): the video tokens
+    in tile-major order, then the text tokens (indices N .. N+T-1) unchanged."""
+    perm_video = np.asarray(perm_video, dtype=np.int64)
+    n = perm_video.shape[0]
+    return np.concatenate([perm_video, np.arange(n, n + text_tokens, dtype=np.int64)])
 
 
 def block_bounds(N: int, b: int):
@@ -147,10 +159,43 @@ def entropy_online(q, k, v, kv_tile: int):
 def token_budget(H, tau: float, N: int) -> np.ndarray:
     """K_hat = ceil(tau * exp(H)) (Sec. 3.1, Eq. 8; App. C.1,
     Eq. implementation-budget-radius), in fp64, clamped to the key count
-    range [1, N] (a budget outside it has no meaning)."""
+    range [1, N] (N the number of keys of the row; a budget outside it has no
+    meaning)."""
     H = np.asarray(H, dtype=np.float64)
     k = np.ceil(tau * np.exp(H))
     return np.clip(k, 1, N).astype(np.int64)
+
+
+def normal_quantile(p: float) -> float:
+    """Phi^{-1}(p) of the standard normal (library routine, fp64)."""
+    return NormalDist().inv_cdf(p)
+
+
+def normal_tail(z):
+    """Phibar(z) = 1 - Phi(z) = erfc(z / sqrt 2) / 2 (fp64)."""
+    return 0.5 * erfc(np.asarray(z, dtype=np.float64) / math.sqrt(2.0))
+
+
+def lognormal_top_mass(q, sigma):
+    """L_LN(q) = Phibar(Phi^{-1}(1 - q) - sigma): the expected share of the total
+    held by the largest fraction q of Lognormal(mu, sigma^2) samples (App. B,
+    "Entropy-identified Lognormal mapping")."""
+    q = np.asarray(q, dtype=np.float64)
+    zq = np.vectorize(lambda a: NormalDist().inv_cdf(a))(1.0 - q)
+    return normal_tail(zq - np.asarray(sigma, dtype=np.float64))
+
+
+def token_budget_lognormal(H, tau: float, S: int) -> np.ndarray:
+    """Lognormal entropy-to-budget mapping (App. B): the weights of a row of S
+    keys are modelled as Lognormal(mu, sigma^2); entropy fixes
+    sigma = sqrt(2 (log S - H)) (H = log S - sigma^2 / 2), and the retained
+    fraction solving L_LN(q) = tau is B = Phibar(sigma - Phi^{-1}(tau)).  The key
+    budget is ceil(S * B) in fp64, clamped to [1, S] (H above log S, possible
+    only by rounding, is taken as log S)."""
+    H = np.asarray(H, dtype=np.float64)
+    sigma = np.sqrt(2.0 * np.maximum(0.0, math.log(S) - H))
+    k = np.ceil(S * normal_tail(sigma - normal_quantile(tau)))
+    return np.clip(k, 1, S).astype(np.int64)
 
 
 # ====================================================== budget -> radius
@@ -180,6 +225,26 @@ def within_radius(D, n, delta, gamma: float):
     with np.errstate(invalid="ignore"):
         rho = r * np.exp(-gamma * np.asarray(delta, dtype=np.float64))
     return np.sqrt(D) <= rho
+
+
+def threshold_table_1d(ncap: int, F: int, gamma: float) -> np.ndarray:
+    """thr1[n, delta] = floor(((pi/2) n) exp(-gamma delta)): the sequence-distance
+    ablation (App. C.1, Eq. area-matched-1d) replaces d_s by |i - j| and the
+    radius by rho_1D = (pi/2) rho_2D^2 = (pi/2) n, so an integer distance passes
+    iff |i - j| <= thr1[n, delta]."""
+    n = np.arange(ncap + 1, dtype=np.float64)[:, None]
+    delta = np.arange(F, dtype=np.float64)[None, :]
+    return np.floor((math.pi / 2.0 * n) * np.exp(-gamma * delta)).astype(np.int64)
+
+
+def within_radius_1d(dr, n, delta, gamma: float):
+    """The 1-D test literally, in fp64: |dr| <= (pi/2) n exp(-gamma delta), the
+    FULL radius infinite."""
+    n = np.asarray(n)
+    r = np.where(n == RADIUS_FULL, np.inf, (math.pi / 2.0) * n.astype(np.float64))
+    with np.errstate(invalid="ignore"):
+        rho = r * np.exp(-gamma * np.asarray(delta, dtype=np.float64))
+    return np.abs(np.asarray(dr, dtype=np.float64)) <= rho
 
 
 def grid_count_bruteforce(i: int, n: int, F: int, H: int, W: int, gamma: float) -> int:
@@ -256,49 +321,77 @@ def analytic_radius(khat, f, F: int, gamma: float) -> np.ndarray:
 
 
 # ====================================================== radius -> masks
-def token_mask_rows(rows, n_rows, F: int, H: int, W: int, gamma: float, keys=None):
-    """M_ij = [d_s(i, j) <= r_i phi(|f_j - f_i|)] (Sec. 3.2, Eq. 15) for query
-    rows ``rows`` (raster indices) with squared radii ``n_rows``, against keys
-    ``keys`` (raster indices, default all).  Returns a bool torch tensor."""
+def token_mask_rows(rows, n_rows, F: int, H: int, W: int, gamma: float, keys=None,
+                    distance: str = "2d"):
+    """M_ij for video query rows ``rows`` (raster indices) with squared radii
+    ``n_rows`` against keys ``keys`` (token indices, default all video tokens).
+    Video keys: M_ij = [d_s(i, j) <= r_i phi(|f_j - f_i|)] (Sec. 3.2, Eq. 15), or
+    for distance "1d" the sequence-distance ablation |i - j| <= (pi/2) n_i
+    phi(|f_j - f_i|) (App. C.1).  Text keys (index >= F*H*W) are always visible
+    (Sec. 3.2: all text keys remain visible).  Returns a bool torch tensor."""
+    N = F * H * W
     f, x, y = grid_coords(F, H, W)
     rows = np.asarray(rows, dtype=np.int64)
-    keys = np.arange(F * H * W) if keys is None else np.asarray(keys, dtype=np.int64)
+    keys = np.arange(N) if keys is None else np.asarray(keys, dtype=np.int64)
+    text = keys >= N
+    kv = np.where(text, 0, keys)
     fr, xr, yr = (torch.as_tensor(a[rows])[:, None] for a in (f, x, y))
-    fk, xk, yk = (torch.as_tensor(a[keys])[None, :] for a in (f, x, y))
-    D = ((xr - xk) ** 2 + (yr - yk) ** 2).to(torch.float64)
+    fk, xk, yk = (torch.as_tensor(a[kv])[None, :] for a in (f, x, y))
     delta = (fr - fk).abs().to(torch.float64)
     n = torch.as_tensor(np.asarray(n_rows, dtype=np.int64))
-    r = torch.where(n == RADIUS_FULL, torch.tensor(math.inf, dtype=torch.float64),
-                    torch.sqrt(n.to(torch.float64)))[:, None]
-    return torch.sqrt(D) <= r * torch.exp(-gamma * delta)
+    full = (n == RADIUS_FULL)[:, None]
+    if distance == "2d":
+        D = ((xr - xk) ** 2 + (yr - yk) ** 2).to(torch.float64)
+        r = torch.where(n == RADIUS_FULL, torch.tensor(math.inf, dtype=torch.float64),
+                        torch.sqrt(n.to(torch.float64)))[:, None]
+        m = torch.sqrt(D) <= r * torch.exp(-gamma * delta)
+    elif distance == "1d":
+        dr = (torch.as_tensor(rows)[:, None] - torch.as_tensor(kv)[None, :]).abs().to(torch.float64)
+        r = torch.where(n == RADIUS_FULL, torch.tensor(math.inf, dtype=torch.float64),
+                        (math.pi / 2.0) * n.to(torch.float64))[:, None]
+        m = dr <= r * torch.exp(-gamma * delta)
+    else:
+        raise ValueError(distance)
+    return (m | full) | torch.as_tensor(text)[None, :]
 
 
 def block_mask_rows(n_raster, perm, b: int, F: int, H: int, W: int, gamma: float,
-                    blocks, rule: str = "vote"):
+                    blocks, rule: str = "vote", distance: str = "2d"):
     """Block-mask rows M[u, :] of Alg. 1 (App. C.1) for the query blocks
-    ``blocks``, from per-token squared radii ``n_raster`` (raster order).
+    ``blocks``, from per-token squared radii ``n_raster`` (token order).
 
-    For a query block u and key block v (tile-major positions), every valid key
-    column j of v gets the count c_j of valid queries i of u with M_ij = 1
-    (Eq. 15).  C = {j : c_j > 0}, C_hi = {j : c_j > n_u / 3}.
+    ``perm`` is the sequence order (tile-major video tokens, then any text
+    tokens); blocks are b consecutive positions of it.  For a video query block
+    u and a video key block v, every valid key column j of v gets the count c_j
+    of valid queries i of u with M_ij = 1 (Eq. 15, or the 1-D test).
+    C = {j : c_j > 0}, C_hi = {j : c_j > n_u / 3}.
     vote:  retained iff |C| > 0 and 10 |C_hi| > 6 |C|   (Alg. 1);
     union: retained iff |C| > 0.
     The diagonal block (u, u) is always retained (every query keeps its own key).
-    n_u is the number of valid queries of u, which equals b except for the last
-    block; the high-coverage test is written 3 c_j > n_u.
-    Returns a bool array (len(blocks), NB).
+    Joint text-video attention (Alg. 1, u >= B_v or v >= B_v): a block holding
+    any text token is retained in every row, and its own row retains every
+    block (reading: a block mixing the last video tokens with the first text
+    tokens counts as a text block, so every text key stays visible).
+    n_u is the number of valid queries of u; the high-coverage test is written
+    3 c_j > n_u.  Returns a bool array (len(blocks), NB).
     """
     perm = np.asarray(perm, dtype=np.int64)
-    N = perm.shape[0]
-    nb = -(-N // b)
+    S = perm.shape[0]
+    N = F * H * W
+    nb = -(-S // b)
+    text_block = np.array([min(S, (v + 1) * b) > N for v in range(nb)])
     out = np.zeros((len(blocks), nb), dtype=bool)
-    pad = nb * b - N
+    pad = nb * b - S
     for r, u in enumerate(blocks):
-        lo, hi = u * b, min((u + 1) * b, N)
+        if text_block[u]:
+            out[r] = True
+            continue
+        lo, hi = u * b, min((u + 1) * b, S)
         rows = perm[lo:hi]
         n_u = hi - lo
-        M = token_mask_rows(rows, np.asarray(n_raster)[rows], F, H, W, gamma, keys=perm)
-        c = M.sum(dim=0).numpy()                       # per key column, tile-major
+        M = token_mask_rows(rows, np.asarray(n_raster)[rows], F, H, W, gamma, keys=perm,
+                            distance=distance)
+        c = M.sum(dim=0).numpy()                       # per key column, sequence order
         c = np.concatenate([c, np.zeros(pad, dtype=c.dtype)]).reshape(nb, b)
         nonempty = (c > 0).sum(axis=1)
         high = (3 * c > n_u).sum(axis=1)
@@ -309,6 +402,7 @@ def block_mask_rows(n_raster, perm, b: int, F: int, H: int, W: int, gamma: float
         else:
             raise ValueError(rule)
         keep[u] = True
+        keep[text_block] = True
         out[r] = keep
     return out
 

@@ -22,6 +22,12 @@ budgets of Sec. 3.1.  Values are rounded once to the workload dtype (fp32, or
 bf16 with round-to-nearest-even); the oracle and the kernels see the identical
 rounded values.
 
+Joint text-video workloads (Sec. 3.2) append ``text_tokens`` text tokens after
+the N video tokens: their 64 features are i.i.d. N(0, 1) (unit variance like the
+Fourier features, no spatial structure), with the same per-head projections,
+per-query scale and noise; they are drawn after all of the head's video values,
+so the video part of a workload does not depend on the text length.
+
 Each head is drawn from its own stream, SeedSequence([seed, head]), so heads can
 be generated in parallel and any subset of heads reproduced on its own.
 """
@@ -58,10 +64,15 @@ class Workload:
     seed: int = 1000
     tile_h: int = 8
     tile_w: int = 8
+    text_tokens: int = 0  # joint text-video attention: text tokens after the video
+
+    @property
+    def n_video(self) -> int:
+        return self.frames * self.height * self.width
 
     @property
     def n_tokens(self) -> int:
-        return self.frames * self.height * self.width
+        return self.n_video + self.text_tokens
 
     @property
     def n_blocks(self) -> int:
@@ -84,6 +95,11 @@ WORKLOADS = {
                              0.1, 8.0, 0.95, seed=1003, tile_h=8, tile_w=16),
     "reuse_480p": Workload("reuse_480p", 1, 12, 128, "bf16", 21, 30, 52, 128,
                            0.25, 4.0, 0.6, seed=1004, tile_h=8, tile_w=16),
+    # joint text-video attention at the HunyuanVideo 720p shape with 256 text
+    # tokens (the paper gives no text length; 256 is a text-encoder length)
+    "hunyuan_joint_720p": Workload("hunyuan_joint_720p", 1, 24, 128, "bf16", 33, 45, 80, 128,
+                                   0.1, 8.0, 0.95, seed=1005, tile_h=8, tile_w=16,
+                                   text_tokens=256),
 }
 
 
@@ -132,7 +148,7 @@ def generate_head(w: Workload, batch_index: int, head: int, feats=None,
     returned as well (used by the drifting reuse sequence)."""
     if feats is None:
         feats = _features(w)
-    n, d = w.n_tokens, w.head_dim
+    n, d = w.n_video, w.head_dim
     rng = np.random.default_rng(np.random.SeedSequence([w.seed, batch_index, head]))
     wq = rng.normal(0.0, 0.125, size=(d, 64)).astype(np.float32)
     wk = rng.normal(0.0, 0.125, size=(d, 64)).astype(np.float32)
@@ -145,6 +161,19 @@ def generate_head(w: Workload, batch_index: int, head: int, feats=None,
     q *= s[:, None]
     k *= 0.5
     k += feats @ wk.T
+    if w.text_tokens:
+        t = w.text_tokens
+        pt = rng.standard_normal((t, 64), dtype=np.float32)
+        st = np.exp(rng.uniform(np.log(w.s_min), np.log(w.s_max), size=t)).astype(np.float32)
+        qt = rng.standard_normal((t, d), dtype=np.float32)
+        kt = rng.standard_normal((t, d), dtype=np.float32)
+        vt = rng.standard_normal((t, d), dtype=np.float32)
+        qt *= 0.5
+        qt += pt @ wq.T
+        qt *= st[:, None]
+        kt *= 0.5
+        kt += pt @ wk.T
+        q, k, v = (np.concatenate([a, b]) for a, b in ((q, qt), (k, kt), (v, vt)))
     out = tuple(bf16_bits_from_f32(a) if w.dtype == "bf16" else a for a in (q, k, v))
     if masters:
         return out, (q, k)

@@ -398,3 +398,147 @@ def test_masked_attention_lse_is_log_partition():
                                            return_lse=True)
     s = q[rows] @ k.T / 8.0
     assert np.abs(lse - np.log(np.exp(s).sum(axis=1))).max() < 1e-12
+
+
+# ------------------------------------------------------- lognormal budget (App. B)
+@pytest.mark.parametrize("S", [256, 32760, 75600, 119056])
+def test_lognormal_budget_at_max_entropy_is_tau_s(S):
+    """At H = log S the fitted sigma is 0 (equal weights), Phibar(-Phi^{-1}(tau))
+    = tau, so the lognormal budget is ceil(tau S): the uniform mapping's value."""
+    H = math.log(S)
+    assert int(O.token_budget_lognormal(H, 0.9, S)) == math.ceil(0.9 * S)
+    # the uniform form evaluates tau * exp(log S) in fp64, which can land just
+    # above an integer tau S (S = 75600: 68040.00000000006)
+    uni = int(O.token_budget(H, 0.9, S))
+    tau_s = 0.9 * S
+    assert uni == math.ceil(tau_s) or (tau_s == round(tau_s) and uni == tau_s + 1)
+
+
+def test_lognormal_budget_inverts_top_mass():
+    """B = Phibar(sigma - Phi^{-1}(tau)) solves L_LN(B) = tau (App. B): with
+    Phi^{-1}(1 - B) = sigma - Phi^{-1}(tau), L_LN(B) = Phibar(-Phi^{-1}(tau))."""
+    z = O.normal_quantile(0.9)
+    for sigma in (0.0, 0.3, 1.0, 2.5, 4.0):
+        q = float(O.normal_tail(sigma - z))
+        assert abs(float(O.lognormal_top_mass(q, sigma)) - 0.9) < 1e-12
+
+
+def test_normal_quantile_and_tail_special_values():
+    assert O.normal_quantile(0.5) == 0.0
+    assert abs(float(O.normal_tail(0.0)) - 0.5) < 1e-16
+    assert abs(float(O.normal_tail(1.959963984540054)) - 0.025) < 1e-15
+    for p in (0.1, 0.5, 0.9, 0.99):
+        assert abs(float(O.normal_tail(-O.normal_quantile(p))) - p) < 1e-14
+
+
+@pytest.mark.parametrize("sigma", [0.5, 1.0, 1.5])
+def test_lognormal_mapping_on_lognormal_weights(sigma):
+    """On weights that ARE lognormal the derivation is exact in the large-sample
+    limit: H = log n - sigma^2 / 2 recovers sigma, and the budget is the number
+    of largest weights holding tau of the mass (checked on 400k seeded draws,
+    tolerances from the sampling error)."""
+    rng = np.random.default_rng(7)
+    n = 400_000
+    x = np.exp(rng.normal(0.3, sigma, size=n))
+    p = x / x.sum()
+    H = float(-(p * np.log(p)).sum())
+    assert abs(math.sqrt(2.0 * (math.log(n) - H)) - sigma) < 0.015 * sigma
+    k = int(O.token_budget_lognormal(H, 0.9, n))
+    ps = np.sort(p)[::-1]
+    assert abs(float(ps[:k].sum()) - 0.9) < 0.004
+    true_k = int(np.searchsorted(np.cumsum(ps), 0.9) + 1)
+    assert abs(k / true_k - 1.0) < 0.015
+
+
+def test_lognormal_budget_monotone_and_clamped():
+    S = 75600
+    H = np.linspace(-5.0, math.log(S) + 1.0, 400)
+    k = O.token_budget_lognormal(H, 0.9, S)
+    assert np.all(np.diff(k) >= 0)
+    assert k.min() >= 1 and k.max() == math.ceil(0.9 * S)
+
+
+# ------------------------------------------------ sequence-distance ablation (App. C.1)
+def test_threshold_1d_first_column_and_literal_test():
+    """thr1[n, 0] = floor((pi/2) n); and |dr| <= thr1[n, delta] is the literal
+    fp64 test |dr| <= (pi/2) n exp(-gamma delta) for every integer distance."""
+    ncap, F, gamma = 200, 5, 0.6
+    t1 = O.threshold_table_1d(ncap, F, gamma)
+    assert np.array_equal(t1[:, 0], np.floor(np.arange(ncap + 1) * (math.pi / 2)).astype(np.int64))
+    dr = np.arange(0, 400)
+    for n in range(ncap + 1):
+        for d in range(F):
+            lit = O.within_radius_1d(dr, n, d, gamma)
+            assert np.array_equal(lit, dr <= t1[n, d]), (n, d)
+
+
+def test_token_mask_1d_brute_force_tiny():
+    """token_mask_rows(distance="1d") against a loop over raster indices."""
+    F, H, W, gamma = 3, 4, 5, 0.6
+    N = F * H * W
+    rng = np.random.default_rng(3)
+    rows = rng.choice(N, 10, replace=False)
+    n = rng.integers(0, 40, 10)
+    n[0] = O.RADIUS_FULL
+    M = O.token_mask_rows(rows, n, F, H, W, gamma, distance="1d").numpy()
+    for a, (i, ni) in enumerate(zip(rows, n)):
+        for j in range(N):
+            fi, fj = i // (H * W), j // (H * W)
+            want = ni == O.RADIUS_FULL or abs(i - j) <= (math.pi / 2) * ni * math.exp(-gamma * abs(fi - fj))
+            assert M[a, j] == want
+
+
+# -------------------------------------------------------- joint text-video (Sec. 3.2)
+def test_joint_text_keys_visible_and_text_blocks_dense():
+    """Text keys stay visible to every query; a block holding text is kept in
+    every row and its own row keeps every block (Alg. 1)."""
+    F, H, W, gamma, b, T = 2, 8, 8, 0.6, 64, 40
+    N = F * H * W
+    perm = O.joint_order(O.tile_major_order(F, H, W, 8, 8), T)
+    S = N + T
+    n = np.zeros(S, dtype=np.int64)
+    M = O.token_mask_rows(np.arange(N), n[:N], F, H, W, gamma, keys=perm)
+    assert M[:, N:].all()
+    assert M[:, :N].sum() == N * F                 # radius 0: its own (x, y) in every frame
+    nb = -(-S // b)
+    mask = O.block_mask_rows(n, perm, b, F, H, W, gamma, range(nb))
+    video_blocks = N // b
+    assert mask[video_blocks:].all()               # text rows dense
+    assert mask[:, video_blocks:].all()            # text columns kept
+    assert np.array_equal(mask[:video_blocks, :video_blocks], np.eye(video_blocks, dtype=bool))
+
+
+def test_joint_mixed_block_counts_as_text():
+    """N not a multiple of b: the block holding the last video tokens and the
+    first text tokens is a text block (dense row and column)."""
+    F, H, W, gamma, b, T = 1, 5, 13, 0.6, 64, 10      # N = 65: block 1 = 1 video + 10 text
+    N = F * H * W
+    perm = O.joint_order(O.tile_major_order(F, H, W, 8, 8), T)
+    n = np.zeros(N + T, dtype=np.int64)
+    mask = O.block_mask_rows(n, perm, b, F, H, W, gamma, range(2))
+    assert mask.all()
+
+
+def test_joint_without_text_is_video_only():
+    w = synth.workload("tiny")
+    perm = O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w)
+    rng = np.random.default_rng(5)
+    n = rng.integers(0, 60, w.n_video)
+    a = O.block_mask_rows(n, perm, w.block, w.frames, w.height, w.width, w.gamma, range(4))
+    b = O.block_mask_rows(n, O.joint_order(perm, 0), w.block, w.frames, w.height, w.width,
+                          w.gamma, range(4))
+    assert np.array_equal(a, b)
+
+
+def test_joint_all_blocks_kept_is_dense_over_s():
+    """Every block retained: TRA attention over the joint sequence is dense
+    attention over all S keys (Eq. 16 with M = 1)."""
+    rng = np.random.default_rng(11)
+    F, H, W, b, T, d = 1, 8, 8, 64, 20, 16
+    N, S = F * H * W, F * H * W + T
+    q, k, v = (rng.standard_normal((S, d)) for _ in range(3))
+    perm = O.joint_order(O.tile_major_order(F, H, W, 8, 8), T)
+    nb = -(-S // b)
+    rows, o = O.masked_attention_rows(q, k, v, perm, b, range(nb), np.ones((nb, nb), dtype=bool))
+    want = O.dense_attention(q[rows], k, v)
+    assert np.allclose(o, want, atol=1e-12)
