@@ -7,8 +7,10 @@
  *                         accumulated inside an online-softmax pass (App. C.2,
  *                         Alg. 2), optionally fused with the dense output O.
  *   tra_budget_radius     entropy -> budget K_hat = ceil(tau * exp(H))
- *                         (Sec. 3.1, Eq. 8) -> smallest boundary-aware squared
- *                         radius reaching it (Sec. 3.2, Eqs. 13-14).
+ *                         (Sec. 3.1, Eq. 8; or the entropy-identified
+ *                         lognormal mapping of App. B) -> smallest
+ *                         boundary-aware squared radius reaching it
+ *                         (Sec. 3.2, Eqs. 13-14).
  *   tra_build_block_mask  per-token radii -> Boolean query-block x key-block
  *                         mask by the token vote of Alg. 1 (App. C.1), plus
  *                         per-row lists of retained key blocks.
@@ -20,17 +22,21 @@
  * ------------------
  * All tensor arguments are DEVICE pointers to contiguous row-major buffers on
  * the device that was current when the plan was created.  Q, K, V and O are
- * [batch][heads][N][head_dim] with tokens in RASTER order of the F x H x W
- * latent grid, token i = (f*H + x)*W + y (Sec. 2.1).  Element type is bf16
- * (TRA_BF16) or fp32 (TRA_FP32) as set in the config; pointers must be 16-byte
- * aligned.  Per-token arrays (entropy, budget, radius_sq, lse) are
- * [batch][heads][N], raster order.
+ * [batch][heads][S][head_dim].  The first N = F*H*W tokens are the video
+ * tokens in RASTER order of the F x H x W latent grid, token
+ * i = (f*H + x)*W + y (Sec. 2.1); the last text_tokens tokens (S = N +
+ * text_tokens) are the text tokens of joint text-video attention (Sec. 3.2),
+ * in the caller's order.  Element type is bf16 (TRA_BF16) or fp32 (TRA_FP32) as
+ * set in the config; pointers must be 16-byte aligned.  Per-token arrays
+ * (entropy, budget, radius_sq, lse) are [batch][heads][S] in the same order.
  *
  * The library applies the tile-major token order of Sec. 3.3 internally: each
  * frame is cut into tile_h x tile_w tiles (edge tiles clipped), tokens are
- * listed frame by frame, tile by tile, row-major inside a tile, and block u is
- * tile-major positions [u*block, min((u+1)*block, N)).  The number of blocks is
- * NB = ceil(N / block).  Block-level arrays use row index
+ * listed frame by frame, tile by tile, row-major inside a tile; text tokens
+ * follow the video tokens unchanged.  Block u is positions
+ * [u*block, min((u+1)*block, S)) of that order and NB = ceil(S / block) (App. C).
+ * A block holding any text token is a text block.  Block-level arrays use row
+ * index
  * r = (b*heads + h)*NB + u:
  *   mask [batch][heads][NB][NB] uint8 (1 = retained),
  *   cnt  [batch][heads][NB]     int32 (retained key blocks of row r),
@@ -86,6 +92,19 @@ typedef enum { TRA_BF16 = 0, TRA_FP32 = 1 } tra_dtype;
  * Under both rules the diagonal block (u, u) is always kept. */
 typedef enum { TRA_MASK_VOTE = 0, TRA_MASK_UNION = 1 } tra_mask_rule;
 
+/* Entropy-to-budget mapping.  UNIFORM is the paper's K_hat = ceil(tau e^H)
+ * (Sec. 3.1, Eq. 8).  LOGNORMAL is the entropy-identified lognormal mapping of
+ * App. B: with S keys per attention row, sigma = sqrt(2 (log S - H)) and
+ * K_hat = ceil(S * Phibar(sigma - Phi^{-1}(tau))), Phibar = 1 - Phi the
+ * standard normal tail; at H = log S both give ceil(tau S). */
+typedef enum { TRA_BUDGET_UNIFORM = 0, TRA_BUDGET_LOGNORMAL = 1 } tra_budget_map;
+
+/* Distance of the radius test.  D2 is Eq. 15: the 2-D spatial distance against
+ * sqrt(n) phi(delta).  D1 is the sequence-distance ablation (App. C.1,
+ * Eq. area-matched-1d): |i - j| between raster indices against the area-matched
+ * 1-D radius (pi/2) n phi(delta), n the squared 2-D radius. */
+typedef enum { TRA_DIST_2D = 0, TRA_DIST_1D = 1 } tra_distance;
+
 typedef struct tra_config {
   int32_t batch;     /* >= 1                                                  */
   int32_t heads;     /* >= 1                                                  */
@@ -98,7 +117,9 @@ typedef struct tra_config {
   int32_t tile_w;    /* tile columns >= 1 (typ. 8 for b=64, 16 for b=128)     */
   int32_t dtype;     /* tra_dtype                                             */
   int32_t rule;      /* tra_mask_rule                                         */
-  int32_t reserved;  /* must be 0                                             */
+  int32_t budget_map;   /* tra_budget_map                                     */
+  int32_t distance;     /* tra_distance                                       */
+  int32_t text_tokens;  /* T >= 0 text tokens after the video tokens          */
   double tau;        /* target attention mass, 0 < tau < 1 (paper: 0.9)      */
   double gamma;      /* temporal decay rate of phi(delta) = exp(-gamma delta),
                         gamma >= 0 (Eq. 10; 0.6 Wan, 0.95 HunyuanVideo)       */
@@ -109,25 +130,31 @@ typedef struct tra_plan_s* tra_plan;
 /* Validates cfg, builds the shape tables on the host in fp64/integer
  * arithmetic (tile-major permutation, squared-radius thresholds
  * thr[n][delta] = floor(n * exp(-2 gamma delta)) for n in [0, n_cap],
- * n_cap = (H-1)^2 + (W-1)^2, per-block bounding boxes) and copies them to
- * the current device.  *out receives the plan, or NULL on failure. */
+ * n_cap = (H-1)^2 + (W-1)^2, for TRA_DIST_1D also the 1-D thresholds
+ * thr1[n][delta] = floor((pi/2) n * exp(-gamma delta)), per-block bounding
+ * boxes) and copies them to the current device.  *out receives the plan, or
+ * NULL on failure. */
 tra_status tra_plan_create(const tra_config* cfg, tra_plan* out);
 
 /* Frees the plan's device tables.  NULL is accepted. */
 tra_status tra_plan_destroy(tra_plan plan);
 
-/* N = F*H*W, NB = ceil(N / block), n_cap as above.  Any output may be NULL. */
+/* n_tokens = S = F*H*W + text_tokens (the token count of every per-token
+ * tensor), NB = ceil(S / block), n_cap as above.  Any output may be NULL. */
 tra_status tra_plan_dims(tra_plan plan, int32_t* n_tokens, int32_t* n_blocks,
                          int32_t* n_cap);
 
 /* Host-only (no device needed): the plan's tables for cfg, for inspection.
- * perm[N]: raster index of the token at tile-major position p.
- * thr[(n_cap+1) * F]: thr[n*F + delta].
- * blocks[NB * 8]: per block {f_min, f_max, x_min, x_max, y_min, y_max,
- *                 n_valid, 0} over its valid tokens.
+ * perm[S]: token index (raster for video, N + t for text token t) of the
+ *          token at position p of the tile-major order.
+ * thr[(n_cap+1) * F]: thr[n*F + delta] (2-D, squared).
+ * thr1[(n_cap+1) * F]: thr1[n*F + delta] = floor((pi/2) n exp(-gamma delta)).
+ * blocks[NB * 10]: per block {f_min, f_max, x_min, x_max, y_min, y_max,
+ *                 n_video, r_min, r_max, n_text} over its video tokens (r the
+ *                 raster index) and the count of its text tokens.
  * Any array pointer may be NULL; *n_cap_out (may be NULL) gets n_cap. */
 tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
-                                int32_t* blocks, int32_t* n_cap_out);
+                                int32_t* thr1, int32_t* blocks, int32_t* n_cap_out);
 
 /* Message describing the last failure on the calling thread ("" if none). */
 const char* tra_last_error(void);
@@ -135,30 +162,41 @@ const char* tra_last_error(void);
 /* Library version string. */
 const char* tra_version(void);
 
-/* Attention entropy H_i = -sum_j p_ij log p_ij in nats over all N keys
- * (Eq. 2), computed with the online-softmax identity
+/* Attention entropy H_i = -sum_j p_ij log p_ij in nats over all S keys
+ * (Eq. 2; with text tokens the joint attention row), for every token, computed
+ * with the online-softmax identity
  * H = log Z - sum_j p_ij s_ij of App. C.2 (Alg. 2).
  * q, k: inputs.  v, o: both NULL (entropy only), or both non-NULL, in which
  * case o also receives dense attention softmax(q k^T / sqrt(d)) v, bitwise equal
  * to tra_dense_attention's output (the fused warm-up step of Alg. 2).
- * entropy: fp32 [batch][heads][N] output. */
+ * entropy: fp32 [batch][heads][S] output. */
 tra_status tra_entropy(tra_plan plan, const void* q, const void* k, const void* v,
                        void* o, float* entropy, void* stream);
 
 /* Entropy -> budget -> squared radius, per token (Sec. 3.1-3.2; App. C.1,
  * Eq. implementation-budget-radius).
- * K_hat = min(max(ceil(tau * exp((double)H)), 1), N) evaluated in fp64.
- * radius_sq = the smallest n in [0, n_cap] whose boundary-aware count
- * C(n) = sum_t #{(x', y') : (x-x')^2 + (y-y')^2 <= thr[n][|t - f|]} (Eq. 13)
- * reaches K_hat (Eq. 14), else TRA_RADIUS_FULL.  Counts are exact integers.
+ * For a video token, K_hat is evaluated in fp64 by the plan's mapping and
+ * clamped to [1, S]:
+ *   UNIFORM    K_hat = ceil(tau * exp(H));
+ *   LOGNORMAL  K_hat = ceil(S * 0.5 erfc((sigma - z) / sqrt 2)),
+ *              sigma = sqrt(2 max(0, log S - H)), z = Phi^{-1}(tau)
+ *              (z found on the host by bisection on Phi to full fp64 precision).
+ * A NaN entropy gives K_hat = S.  radius_sq = the smallest n in [0, n_cap] whose
+ * boundary-aware count C(n) = sum_t #{(x', y') : (x-x')^2 + (y-y')^2 <=
+ * thr[n][|t - f|]} over the video grid (Eq. 13) reaches K_hat (Eq. 14), else
+ * TRA_RADIUS_FULL.  Counts are exact integers.  Text tokens get K_hat = S and
+ * TRA_RADIUS_FULL.
  * entropy: fp32 input; budget: int32 output or NULL; radius_sq: int32 output. */
 tra_status tra_budget_radius(tra_plan plan, const float* entropy, int32_t* budget,
                              int32_t* radius_sq, void* stream);
 
-/* Alg. 1 block mask from per-token squared radii (raster order).  A query i
- * covers key j iff (x_i-x_j)^2 + (y_i-y_j)^2 <= thr[n_i][|f_i - f_j|]
- * (Eq. 15); radius values outside [0, n_cap] other than TRA_RADIUS_FULL are
- * clamped (negative -> 0, larger -> FULL).  The rule comes from the plan.
+/* Alg. 1 block mask from per-token squared radii (raster order).  A video
+ * query i covers a video key j iff (x_i-x_j)^2 + (y_i-y_j)^2 <=
+ * thr[n_i][|f_i - f_j|] (Eq. 15), or for TRA_DIST_1D iff |i - j| <=
+ * thr1[n_i][|f_i - f_j|]; radius values outside [0, n_cap] other than
+ * TRA_RADIUS_FULL are clamped (negative -> 0, larger -> FULL).  The rule and
+ * distance come from the plan.  Text blocks are retained in every row and a
+ * text block's row retains every block (Alg. 1; text keys stay visible). 
  * mask: uint8 output or NULL; cnt, cols: int32 outputs; order: int32 output
  * (the heaviest-first row order, sorted in the plan's sort workspace) or NULL
  * (not computed). */

@@ -30,6 +30,10 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtra.so")
 TRA_RADIUS_FULL = 2 ** 31 - 1
 TRA_BF16, TRA_FP32 = 0, 1
 TRA_MASK_VOTE, TRA_MASK_UNION = 0, 1
+TRA_BUDGET_UNIFORM, TRA_BUDGET_LOGNORMAL = 0, 1
+TRA_DIST_2D, TRA_DIST_1D = 0, 1
+_BUDGET = {"uniform": TRA_BUDGET_UNIFORM, "lognormal": TRA_BUDGET_LOGNORMAL}
+_DIST = {"2d": TRA_DIST_2D, "1d": TRA_DIST_1D}
 
 EXPORTED_SYMBOLS = (
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
@@ -50,7 +54,7 @@ class TraError(RuntimeError):
 class _Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "batch", "heads", "frames", "height", "width", "head_dim", "block",
-        "tile_h", "tile_w", "dtype", "rule", "reserved")] + [
+        "tile_h", "tile_w", "dtype", "rule", "budget_map", "distance", "text_tokens")] + [
         ("tau", ctypes.c_double), ("gamma", ctypes.c_double)]
 
 
@@ -70,10 +74,17 @@ class Config:
     rule: str = "vote"        # "vote" (Alg. 1) or "union"
     tau: float = 0.9
     gamma: float = 0.6
+    budget: str = "uniform"   # "uniform" (Eq. 8) or "lognormal" (App. B)
+    distance: str = "2d"      # "2d" (Eq. 15) or "1d" (sequence-distance ablation)
+    text_tokens: int = 0      # text tokens after the video tokens (joint attention)
+
+    @property
+    def n_video(self) -> int:
+        return self.frames * self.height * self.width
 
     @property
     def n_tokens(self) -> int:
-        return self.frames * self.height * self.width
+        return self.n_video + self.text_tokens
 
     @property
     def n_blocks(self) -> int:
@@ -84,13 +95,15 @@ class Config:
                        self.head_dim, self.block, self.tile_h, self.tile_w,
                        TRA_BF16 if self.dtype == "bf16" else TRA_FP32 if self.dtype == "fp32" else 99,
                        TRA_MASK_VOTE if self.rule == "vote" else TRA_MASK_UNION if self.rule == "union" else 99,
-                       0, self.tau, self.gamma)
+                       _BUDGET.get(self.budget, 99), _DIST.get(self.distance, 99), self.text_tokens,
+                       self.tau, self.gamma)
 
     @classmethod
     def from_workload(cls, w, **kw) -> "Config":
         base = dict(batch=w.batch, heads=w.heads, frames=w.frames, height=w.height,
                     width=w.width, head_dim=w.head_dim, block=w.block, tile_h=w.tile_h,
-                    tile_w=w.tile_w, dtype=w.dtype, tau=w.tau, gamma=w.gamma)
+                    tile_w=w.tile_w, dtype=w.dtype, tau=w.tau, gamma=w.gamma,
+                    text_tokens=getattr(w, "text_tokens", 0))
         base.update(kw)
         return cls(**base)
 
@@ -111,7 +124,7 @@ def lib() -> ctypes.CDLL:
     L.tra_plan_create.argtypes = [cfgp, ctypes.POINTER(P)]
     L.tra_plan_destroy.argtypes = [P]
     L.tra_plan_dims.argtypes = [P, P, P, P]
-    L.tra_plan_host_tables.argtypes = [cfgp, P, P, P, P]
+    L.tra_plan_host_tables.argtypes = [cfgp, P, P, P, P, P]
     L.tra_last_error.restype = ctypes.c_char_p
     L.tra_version.restype = ctypes.c_char_p
     L.tra_entropy.argtypes = [P, V, V, V, V, V, V]
@@ -189,16 +202,18 @@ def tra_plan_dims(plan: Plan):
 
 
 def tra_plan_host_tables(cfg: Config):
-    """Host-only tables of cfg: (perm[N], thr[(n_cap+1), F], blocks[NB, 8], n_cap)."""
+    """Host-only tables of cfg:
+    (perm[S], thr[(n_cap+1), F], thr1[(n_cap+1), F], blocks[NB, 10], n_cap)."""
     c = cfg.to_c()
     cap = ctypes.c_int32()
-    _check(lib().tra_plan_host_tables(ctypes.byref(c), None, None, None, ctypes.byref(cap)))
+    _check(lib().tra_plan_host_tables(ctypes.byref(c), None, None, None, None, ctypes.byref(cap)))
     perm = np.empty(cfg.n_tokens, dtype=np.int32)
     thr = np.empty((cap.value + 1, cfg.frames), dtype=np.int32)
-    blocks = np.empty((cfg.n_blocks, 8), dtype=np.int32)
+    thr1 = np.empty((cap.value + 1, cfg.frames), dtype=np.int32)
+    blocks = np.empty((cfg.n_blocks, 10), dtype=np.int32)
     _check(lib().tra_plan_host_tables(ctypes.byref(c), perm.ctypes.data, thr.ctypes.data,
-                                      blocks.ctypes.data, ctypes.byref(cap)))
-    return perm, thr, blocks, cap.value
+                                      thr1.ctypes.data, blocks.ctypes.data, ctypes.byref(cap)))
+    return perm, thr, thr1, blocks, cap.value
 
 
 # ------------------------------------------------------------------ marshalling

@@ -76,15 +76,17 @@ const char* tra_last_error(void) { return g_last_error.c_str(); }
 const char* tra_version(void) { return "tra-mi355x 0.1 (gfx950)"; }
 
 tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
-                                int32_t* blocks, int32_t* n_cap_out) {
+                                int32_t* thr1, int32_t* blocks, int32_t* n_cap_out) {
   try {
     std::string why;
     tra_status s = tra::validate_config(cfg, &why);
     if (s != TRA_OK) return fail(s, why);
     tra::HostTables t;
-    tra::build_host_tables(*cfg, &t, perm != nullptr, thr != nullptr, blocks != nullptr);
+    tra::build_host_tables(*cfg, &t, perm != nullptr, thr != nullptr, thr1 != nullptr,
+                           blocks != nullptr);
     if (perm) std::memcpy(perm, t.perm.data(), t.perm.size() * sizeof(int32_t));
     if (thr) std::memcpy(thr, t.thr.data(), t.thr.size() * sizeof(int32_t));
+    if (thr1) std::memcpy(thr1, t.thr1.data(), t.thr1.size() * sizeof(int32_t));
     if (blocks) std::memcpy(blocks, t.blocks.data(), t.blocks.size() * sizeof(int32_t));
     if (n_cap_out) *n_cap_out = t.n_cap;
     return ok();
@@ -103,6 +105,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_perm);
   (void)hipFree(p->d_coord);
   (void)hipFree(p->d_thr);
+  (void)hipFree(p->d_thr1);
   (void)hipFree(p->d_blocks);
   (void)hipFree(p->d_sort_ws);
   (void)hipFree(p->d_kt);
@@ -130,13 +133,16 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       return fail(TRA_ERR_UNSUPPORTED, std::string("device is ") + prop.gcnArchName + ", not gfx950");
 
     tra::HostTables t;
-    tra::build_host_tables(*cfg, &t, true, true, true);
+    const bool one_d = cfg->distance == TRA_DIST_1D;
+    tra::build_host_tables(*cfg, &t, true, true, one_d, true);
 
     tra_plan p = new tra_plan_s();
     p->cfg = *cfg;
     p->device = dev;
     p->N = t.N;
+    p->S = t.S;
     p->NB = t.NB;
+    p->z_tau = tra::normal_quantile(cfg->tau);
     p->n_cap = t.n_cap;
     p->rows = cfg->batch * cfg->heads * t.NB;
     p->sort_chunks = (p->rows + tra::kSortChunk - 1) / tra::kSortChunk;
@@ -153,6 +159,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
         (e = upload(&p->d_coord, t.coord)) != hipSuccess ||
         (e = upload(&p->d_thr, t.thr)) != hipSuccess ||
         (e = upload(&p->d_blocks, t.blocks)) != hipSuccess ||
+        (one_d && (e = upload(&p->d_thr1, t.thr1)) != hipSuccess) ||
         (e = hipMalloc((void**)&p->d_sort_ws, p->sort_ws_elems * sizeof(int32_t))) != hipSuccess) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
@@ -176,7 +183,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
 
 tra_status tra_plan_dims(tra_plan p, int32_t* n_tokens, int32_t* n_blocks, int32_t* n_cap) {
   if (!p) return fail(TRA_ERR_INVALID_ARG, "plan is NULL");
-  if (n_tokens) *n_tokens = p->N;
+  if (n_tokens) *n_tokens = p->S;
   if (n_blocks) *n_blocks = p->NB;
   if (n_cap) *n_cap = p->n_cap;
   return ok();

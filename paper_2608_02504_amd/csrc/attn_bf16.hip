@@ -521,7 +521,7 @@ void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const size_t list_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
   hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), list_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
-                     a.cnt, a.cols, a.order, p.N, p.n_pad, p.NB, p.rows, scale_log2);
+                     a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2);
 }
 
 template <int D>
@@ -530,12 +530,12 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
   const int bhs = p.cfg.batch * p.cfg.heads;
   const long long total = (long long)bhs * p.n_pad * ch;
   hipLaunchKernelGGL(gather_k_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     (const uint4*)a.k, (uint4*)p.d_kt, p.d_perm, p.N, p.n_pad, ch, total);
+                     (const uint4*)a.k, (uint4*)p.d_kt, p.d_perm, p.S, p.n_pad, ch, total);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.v) {
     hipLaunchKernelGGL((gather_vt_kernel<D>), dim3(p.n_pad / 64, bhs), dim3(256), 0, s,
-                       (const uint16_t*)a.v, p.d_vt, p.d_perm, p.N, p.n_pad);
+                       (const uint16_t*)a.v, p.d_vt, p.d_perm, p.S, p.n_pad);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

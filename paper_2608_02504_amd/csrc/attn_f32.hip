@@ -122,7 +122,7 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
 template <int D, int B>
 hipError_t launch_f32_db(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   F32Params P{(const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.o, a.lse,
-              a.entropy, p.d_perm, a.cnt, a.cols, a.order, p.N, p.NB, p.rows,
+              a.entropy, p.d_perm, a.cnt, a.cols, a.order, p.S, p.NB, p.rows,
               1.0f / sqrtf((float)D)};
   const dim3 grid(p.rows), block(B);
   if (a.sparse)

@@ -11,6 +11,15 @@
 // favourable frame is inside.  Only "partial" queries are tested key by key,
 // so the counts -- and the mask -- are exactly Alg. 1's; the boxes only skip
 // work whose outcome is already known.  Everything is integer arithmetic.
+//
+// Sequence-distance ablation (DIST = TRA_DIST_1D, App. C.1): a query covers
+// key j iff |i - j| <= thr1[n_i][|f_i - f_j|] on raster indices; the box of a
+// block is then its raster-index range, and the same none / all / partial
+// argument holds because thr1 is non-increasing in delta too.
+//
+// Joint text-video attention (Sec. 3.2; Alg. 1's u >= B_v or v >= B_v branch):
+// a block holding any text token is retained in every row, and the row of such
+// a block retains every key block.
 #include <climits>
 
 #include "tra_internal.h"
@@ -21,14 +30,35 @@ namespace {
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
 
-template <int B, int RULE>
+// Distance of a token pair from its position difference: squared Euclidean
+// (x, y) for 2-D, |raster difference| (carried in the first component) for 1-D.
+template <int DIST>
+__device__ __forceinline__ int metric(int da, int db) {
+  if constexpr (DIST == TRA_DIST_1D) return abs(da);
+  else return da * da + db * db;
+}
+
+// Position of a packed coordinate in the metric's space.
+template <int DIST>
+__device__ __forceinline__ void position(int32_t c, int H, int W, int* a, int* b, int* f) {
+  *f = coord_f(c);
+  if constexpr (DIST == TRA_DIST_1D) {
+    *a = (*f * H + coord_x(c)) * W + coord_y(c);
+    *b = 0;
+  } else {
+    *a = coord_x(c);
+    *b = coord_y(c);
+  }
+}
+
+template <int B, int RULE, int DIST>
 __global__ __launch_bounds__(256) void block_mask_kernel(
     const int32_t* __restrict__ radius_sq, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ coord, const int32_t* __restrict__ thr,
     const int32_t* __restrict__ binfo, uint8_t* __restrict__ mask, int32_t* __restrict__ cnt,
-    int32_t* __restrict__ cols, int N, int NB, int F, int n_cap) {
+    int32_t* __restrict__ cols, int N, int S, int NB, int F, int H, int W, int n_cap) {
   constexpr int QPL = B / 64;  // queries (and keys) per lane
-  __shared__ int32_t s_T[B * kMaxFrames];  // s_T[q*F + delta]: squared-distance threshold of query q
+  __shared__ int32_t s_T[B * kMaxFrames];  // s_T[q*F + delta]: distance threshold of query q
   __shared__ int32_t s_c[B];               // packed coordinate of query q
   __shared__ uint8_t s_keep[kMaxBlocks];
 
@@ -36,12 +66,22 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
   const int bh = row / NB, u = row - bh * NB;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int q0 = u * B;
+
+  if (min(S, q0 + B) > N) {
+    // a text block's row keeps every key block
+    for (int v = t; v < NB; v += blockDim.x) {
+      if (mask) mask[(size_t)row * NB + v] = 1;
+      cols[(size_t)row * NB + v] = v;
+    }
+    if (t == 0) cnt[row] = NB;
+    return;
+  }
   const int n_u = min(B, N - q0);
 
   for (int qi = t; qi < B; qi += blockDim.x) {
     if (qi < n_u) {
       const int pos = q0 + qi;
-      int n = radius_sq[(size_t)bh * N + perm[pos]];
+      int n = radius_sq[(size_t)bh * S + perm[pos]];
       const bool full = n > n_cap;  // TRA_RADIUS_FULL and anything above the cap
       n = max(n, 0);
       s_c[qi] = coord[pos];
@@ -53,14 +93,13 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
   }
   __syncthreads();
 
-  // This lane's queries, fixed for the whole row.
+  // This lane's queries, fixed for the whole row (positions in the metric's space).
   int qx[QPL], qy[QPL], qf[QPL];
   bool qvalid[QPL];
 #pragma unroll
   for (int s = 0; s < QPL; ++s) {
     const int qi = lane + 64 * s;
-    const int c = s_c[qi];
-    qx[s] = coord_x(c); qy[s] = coord_y(c); qf[s] = coord_f(c);
+    position<DIST>(s_c[qi], H, W, &qx[s], &qy[s], &qf[s]);
     qvalid[s] = qi < n_u;
   }
 
@@ -68,10 +107,13 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
     bool keep;
     if (v == u) {
       keep = true;  // every query keeps its own key, so the diagonal block is never empty
+    } else if (min(S, (v + 1) * B) > N) {
+      keep = true;  // text keys stay visible
     } else {
       const int32_t* bi = binfo + (size_t)v * kBlockInfo;
-      const int fmin = bi[0], fmax = bi[1], xmin = bi[2], xmax = bi[3];
-      const int ymin = bi[4], ymax = bi[5], n_v = bi[6];
+      const int fmin = bi[0], fmax = bi[1], n_v = bi[6];
+      const int xmin = DIST == TRA_DIST_1D ? bi[7] : bi[2], xmax = DIST == TRA_DIST_1D ? bi[8] : bi[3];
+      const int ymin = DIST == TRA_DIST_1D ? 0 : bi[4], ymax = DIST == TRA_DIST_1D ? 0 : bi[5];
       uint64_t all_m[QPL], part_m[QPL];
       int n_all = 0;
       bool any_part = false;
@@ -86,8 +128,8 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
         const int dmax = max(qf[s] - fmin, fmax - qf[s]);
         const int t_hi = s_T[qi * F + dmin];  // thresholds are non-increasing in delta
         const int t_lo = s_T[qi * F + dmax];
-        const bool none = !qvalid[s] || dxn * dxn + dyn * dyn > t_hi;
-        const bool all = qvalid[s] && dxf * dxf + dyf * dyf <= t_lo;
+        const bool none = !qvalid[s] || metric<DIST>(dxn, dyn) > t_hi;
+        const bool all = qvalid[s] && metric<DIST>(dxf, dyf) <= t_lo;
         all_m[s] = ballot(all);
         part_m[s] = ballot(!none && !all);
         n_all += popc(all_m[s]);
@@ -108,7 +150,7 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
           const int j = lane + 64 * s;
           kvalid[s] = j < n_v;
           const int cc = kvalid[s] ? coord[(size_t)v * B + j] : 0;
-          kx[s] = coord_x(cc); ky[s] = coord_y(cc); kf[s] = coord_f(cc);
+          position<DIST>(cc, H, W, &kx[s], &ky[s], &kf[s]);
           c[s] = n_all;
         }
 #pragma unroll
@@ -117,14 +159,14 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
           while (m) {
             const int qi = __ffsll((unsigned long long)m) - 1 + 64 * s2;
             m &= m - 1;
-            const int pc = s_c[qi];
-            const int px = coord_x(pc), py = coord_y(pc), pf = coord_f(pc);
+            int px, py, pf;
+            position<DIST>(s_c[qi], H, W, &px, &py, &pf);
             const int32_t* Tp = s_T + qi * F;
 #pragma unroll
             for (int s = 0; s < QPL; ++s) {
               const int dx = px - kx[s], dy = py - ky[s];
               const int dl = abs(pf - kf[s]);
-              c[s] += (dx * dx + dy * dy <= Tp[dl]) ? 1 : 0;
+              c[s] += (metric<DIST>(dx, dy) <= Tp[dl]) ? 1 : 0;
             }
           }
         }
@@ -223,26 +265,33 @@ __global__ __launch_bounds__(kSortChunk) void order_scatter_kernel(const int32_t
 
 }  // namespace
 
+template <int B, int RULE, int DIST>
+void launch_mask_variant(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask, int32_t* cnt,
+                         int32_t* cols, hipStream_t s) {
+  const int32_t* thr = DIST == TRA_DIST_1D ? p.d_thr1 : p.d_thr;
+  hipLaunchKernelGGL((block_mask_kernel<B, RULE, DIST>), dim3(p.rows), dim3(256), 0, s, radius_sq, p.d_perm,
+                     p.d_coord, thr, p.d_blocks, mask, cnt, cols, p.N, p.S, p.NB, p.cfg.frames,
+                     p.cfg.height, p.cfg.width, p.n_cap);
+}
+
+template <int B, int RULE>
+void launch_mask_dist(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask, int32_t* cnt,
+                      int32_t* cols, hipStream_t s) {
+  if (p.cfg.distance == TRA_DIST_1D) launch_mask_variant<B, RULE, TRA_DIST_1D>(p, radius_sq, mask, cnt, cols, s);
+  else launch_mask_variant<B, RULE, TRA_DIST_2D>(p, radius_sq, mask, cnt, cols, s);
+}
+
+template <int B>
+void launch_mask_rule(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask, int32_t* cnt,
+                      int32_t* cols, hipStream_t s) {
+  if (p.cfg.rule == TRA_MASK_VOTE) launch_mask_dist<B, TRA_MASK_VOTE>(p, radius_sq, mask, cnt, cols, s);
+  else launch_mask_dist<B, TRA_MASK_UNION>(p, radius_sq, mask, cnt, cols, s);
+}
+
 hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask,
                              int32_t* cnt, int32_t* cols, hipStream_t s) {
-  const dim3 grid(p.rows), block(256);
-  const int F = p.cfg.frames;
-  const bool vote = p.cfg.rule == TRA_MASK_VOTE;
-  if (p.cfg.block == 128) {
-    if (vote)
-      hipLaunchKernelGGL((block_mask_kernel<128, TRA_MASK_VOTE>), grid, block, 0, s, radius_sq, p.d_perm,
-                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
-    else
-      hipLaunchKernelGGL((block_mask_kernel<128, TRA_MASK_UNION>), grid, block, 0, s, radius_sq, p.d_perm,
-                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
-  } else {
-    if (vote)
-      hipLaunchKernelGGL((block_mask_kernel<64, TRA_MASK_VOTE>), grid, block, 0, s, radius_sq, p.d_perm,
-                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
-    else
-      hipLaunchKernelGGL((block_mask_kernel<64, TRA_MASK_UNION>), grid, block, 0, s, radius_sq, p.d_perm,
-                         p.d_coord, p.d_thr, p.d_blocks, mask, cnt, cols, p.N, p.NB, F, p.n_cap);
-  }
+  if (p.cfg.block == 128) launch_mask_rule<128>(p, radius_sq, mask, cnt, cols, s);
+  else launch_mask_rule<64>(p, radius_sq, mask, cnt, cols, s);
   return hipGetLastError();
 }
 

@@ -8,9 +8,14 @@
 //    temporal distance delta, the test d_s <= r * phi(delta) of Eq. 15 with
 //    phi(delta) = exp(-gamma delta) (Eq. 10) holds for an integer squared
 //    distance D iff D <= floor(n * exp(-2 gamma delta));
+//  * the sequence-distance ablation (App. C.1, Eq. area-matched-1d): the 1-D
+//    radius is (pi/2) r^2 = (pi/2) n and the test |i - j| <= (pi/2) n phi(delta)
+//    holds for an integer distance iff |i - j| <= floor((pi/2) n exp(-gamma delta));
 //  * per-block bounding boxes used to skip block pairs (App. C.1, "Kernel
 //    execution": a bounding-box test rejects pairs with no valid
-//    interaction).
+//    interaction);
+//  * text tokens of joint text-video attention (Sec. 3.2) follow the video
+//    tokens in the sequence and keep their order.
 #include <algorithm>
 #include <cmath>
 
@@ -26,7 +31,9 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   if (c.frames > kMaxFrames) { *why = "frames > 64 is not supported"; return TRA_ERR_UNSUPPORTED; }
   if (c.height > 1023 || c.width > 1023) { *why = "height and width must be <= 1023"; return TRA_ERR_UNSUPPORTED; }
   if (c.tile_h < 1 || c.tile_w < 1) { *why = "tile_h and tile_w must be >= 1"; return TRA_ERR_INVALID_ARG; }
-  if (c.reserved != 0) { *why = "reserved must be 0"; return TRA_ERR_INVALID_ARG; }
+  if (c.budget_map != TRA_BUDGET_UNIFORM && c.budget_map != TRA_BUDGET_LOGNORMAL) { *why = "unknown budget mapping"; return TRA_ERR_INVALID_ARG; }
+  if (c.distance != TRA_DIST_2D && c.distance != TRA_DIST_1D) { *why = "unknown distance"; return TRA_ERR_INVALID_ARG; }
+  if (c.text_tokens < 0) { *why = "text_tokens must be >= 0"; return TRA_ERR_INVALID_ARG; }
   if (c.dtype != TRA_BF16 && c.dtype != TRA_FP32) { *why = "unknown dtype"; return TRA_ERR_INVALID_ARG; }
   if (c.rule != TRA_MASK_VOTE && c.rule != TRA_MASK_UNION) { *why = "unknown mask rule"; return TRA_ERR_INVALID_ARG; }
   if (!(c.tau > 0.0 && c.tau < 1.0)) { *why = "tau must be in (0, 1)"; return TRA_ERR_INVALID_ARG; }
@@ -34,7 +41,7 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   if (c.head_dim != 64 && c.head_dim != 128) { *why = "head_dim must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
   if (c.block != 64 && c.block != 128) { *why = "block must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
   if (c.dtype == TRA_BF16 && c.block != 128) { *why = "bf16 needs block 128"; return TRA_ERR_UNSUPPORTED; }
-  const int64_t n = (int64_t)c.frames * c.height * c.width;
+  const int64_t n = (int64_t)c.frames * c.height * c.width + c.text_tokens;
   const int64_t nb = (n + c.block - 1) / c.block;
   if (nb > kMaxBlocks) { *why = "more than 4096 blocks per head"; return TRA_ERR_UNSUPPORTED; }
   const int64_t rows = (int64_t)c.batch * c.heads * nb;
@@ -45,28 +52,43 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   return TRA_OK;
 }
 
+double normal_quantile(double p) {
+  // Phi(x) = erfc(-x / sqrt 2) / 2 is increasing; bisect until the bracket
+  // stops shrinking in fp64.
+  double lo = -40.0, hi = 40.0;
+  for (int it = 0; it < 200; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (mid == lo || mid == hi) break;
+    if (0.5 * std::erfc(-mid / std::sqrt(2.0)) < p) lo = mid;
+    else hi = mid;
+  }
+  return 0.5 * (lo + hi);
+}
+
 void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
-                       bool with_thr, bool with_blocks) {
+                       bool with_thr, bool with_thr1, bool with_blocks) {
   const int F = c.frames, H = c.height, W = c.width, b = c.block;
   t->N = F * H * W;
-  t->NB = (t->N + b - 1) / b;
+  t->S = t->N + c.text_tokens;
+  t->NB = (t->S + b - 1) / b;
   t->n_cap = (H - 1) * (H - 1) + (W - 1) * (W - 1);
 
   std::vector<int32_t> perm;
   if (with_perm_coord || with_blocks) {
-    // One frame's tile-major order, then offset per frame.
+    // One frame's tile-major order, then offset per frame; text tokens last.
     std::vector<int32_t> frame;
     frame.reserve((size_t)H * W);
     for (int ty = 0; ty < H; ty += c.tile_h)
       for (int tx = 0; tx < W; tx += c.tile_w)
         for (int x = ty; x < std::min(H, ty + c.tile_h); ++x)
           for (int y = tx; y < std::min(W, tx + c.tile_w); ++y) frame.push_back(x * W + y);
-    perm.resize(t->N);
+    perm.resize(t->S);
     for (int f = 0; f < F; ++f)
       for (int p = 0; p < H * W; ++p) perm[(size_t)f * H * W + p] = f * H * W + frame[p];
+    for (int p = t->N; p < t->S; ++p) perm[p] = p;
   }
   if (with_perm_coord) {
-    t->coord.resize(t->N);
+    t->coord.assign(t->S, 0);
     for (int p = 0; p < t->N; ++p) {
       const int i = perm[p];
       t->coord[p] = pack_coord(i / (H * W), (i / W) % H, i % W);
@@ -81,21 +103,34 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
         t->thr[(size_t)n * F + d] = d == 0 ? n : (int32_t)std::floor((double)n * e);
       }
   }
+  if (with_thr1) {
+    t->thr1.resize((size_t)(t->n_cap + 1) * F);
+    const double half_pi = 1.5707963267948966;  // pi / 2
+    for (int n = 0; n <= t->n_cap; ++n)
+      for (int d = 0; d < F; ++d) {
+        // ((pi/2) n) exp(-gamma delta), floored
+        const double e = std::exp(-c.gamma * (double)d);
+        t->thr1[(size_t)n * F + d] = (int32_t)std::floor((half_pi * (double)n) * e);
+      }
+  }
   if (with_blocks) {
     t->blocks.assign((size_t)t->NB * kBlockInfo, 0);
     for (int u = 0; u < t->NB; ++u) {
       int fmin = F, fmax = -1, xmin = H, xmax = -1, ymin = W, ymax = -1;
-      const int lo = u * b, hi = std::min(t->N, lo + b);
+      int rmin = t->N, rmax = -1;
+      const int lo = u * b, hi_all = std::min(t->S, lo + b), hi = std::min(t->N, hi_all);
       for (int p = lo; p < hi; ++p) {
         const int i = perm[p];
         const int f = i / (H * W), x = (i / W) % H, y = i % W;
         fmin = std::min(fmin, f); fmax = std::max(fmax, f);
         xmin = std::min(xmin, x); xmax = std::max(xmax, x);
         ymin = std::min(ymin, y); ymax = std::max(ymax, y);
+        rmin = std::min(rmin, i); rmax = std::max(rmax, i);
       }
       int32_t* o = &t->blocks[(size_t)u * kBlockInfo];
       o[0] = fmin; o[1] = fmax; o[2] = xmin; o[3] = xmax; o[4] = ymin; o[5] = ymax;
-      o[6] = hi - lo; o[7] = 0;
+      o[6] = std::max(0, hi - lo); o[7] = rmin; o[8] = rmax;
+      o[9] = hi_all - std::max(lo, t->N) > 0 ? hi_all - std::max(lo, t->N) : 0;
     }
   }
   if (with_perm_coord) t->perm = std::move(perm);

@@ -1,6 +1,8 @@
 // Entropy -> budget -> squared radius, one thread per (batch, head, token).
 //
 //  K_hat = ceil(tau * exp(H))                       Sec. 3.1, Eq. 8 (fp64)
+//    or, lognormal mapping (App. B, Eq. lognormal_budget_appendix), with S keys
+//    per row: K_hat = ceil(S * Phibar(sqrt(2 (log S - H)) - Phi^{-1}(tau)))
 //  C(n)  = sum_t #{(x', y') in frame : (x-x')^2 + (y-y')^2 <= thr[n][|t-f|]}
 //                                                   Sec. 3.2, Eq. 13
 //  n     = min{n in [0, n_cap] : C(n) >= K_hat}, else FULL        Eq. 14
@@ -58,16 +60,32 @@ __device__ int grid_count(int f, int x, int y, int n, const int32_t* __restrict_
   return total;
 }
 
+template <int MAP>
 __global__ __launch_bounds__(256) void budget_radius_kernel(
     const float* __restrict__ entropy, int32_t* __restrict__ budget, int32_t* __restrict__ radius_sq,
-    const int32_t* __restrict__ thr, int total, int N, int F, int H, int W, int n_cap, double tau) {
+    const int32_t* __restrict__ thr, int total, int S, int N, int F, int H, int W, int n_cap,
+    double tau, double z_tau) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
-  const int i = idx % N;  // raster token
+  const int i = idx % S;  // token: raster index for video, >= N for text
+  if (i >= N) {
+    // text token: no radius (joint attention keeps its rows dense)
+    if (budget) budget[idx] = S;
+    radius_sq[idx] = TRA_RADIUS_FULL;
+    return;
+  }
   const double h = (double)entropy[idx];
-  const double kd = ceil(tau * exp(h));
+  double kd;
+  if (h != h) {
+    kd = h;  // NaN entropy: keep everything (below)
+  } else if (MAP == TRA_BUDGET_LOGNORMAL) {
+    const double sigma = sqrt(2.0 * fmax(0.0, log((double)S) - h));
+    kd = ceil((double)S * (0.5 * erfc((sigma - z_tau) * 0.70710678118654752)));
+  } else {
+    kd = ceil(tau * exp(h));
+  }
   int khat;
-  if (kd != kd || kd >= (double)N) khat = N;  // NaN entropy: keep everything
+  if (kd != kd || kd >= (double)S) khat = S;  // NaN entropy: keep everything
   else if (kd < 1.0) khat = 1;
   else khat = (int)kd;
   if (budget) budget[idx] = khat;
@@ -94,11 +112,17 @@ __global__ __launch_bounds__(256) void budget_radius_kernel(
 
 hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
                                 int32_t* radius_sq, hipStream_t s) {
-  const int total = p.cfg.batch * p.cfg.heads * p.N;
+  const int total = p.cfg.batch * p.cfg.heads * p.S;
   const int threads = 256;
-  hipLaunchKernelGGL(budget_radius_kernel, dim3((total + threads - 1) / threads), dim3(threads), 0, s,
-                     entropy, budget, radius_sq, p.d_thr, total, p.N, p.cfg.frames, p.cfg.height,
-                     p.cfg.width, p.n_cap, p.cfg.tau);
+  const dim3 grid((total + threads - 1) / threads);
+  if (p.cfg.budget_map == TRA_BUDGET_LOGNORMAL)
+    hipLaunchKernelGGL(budget_radius_kernel<TRA_BUDGET_LOGNORMAL>, grid, dim3(threads), 0, s, entropy,
+                       budget, radius_sq, p.d_thr, total, p.S, p.N, p.cfg.frames, p.cfg.height,
+                       p.cfg.width, p.n_cap, p.cfg.tau, p.z_tau);
+  else
+    hipLaunchKernelGGL(budget_radius_kernel<TRA_BUDGET_UNIFORM>, grid, dim3(threads), 0, s, entropy,
+                       budget, radius_sq, p.d_thr, total, p.S, p.N, p.cfg.frames, p.cfg.height,
+                       p.cfg.width, p.n_cap, p.cfg.tau, p.z_tau);
   return hipGetLastError();
 }
 

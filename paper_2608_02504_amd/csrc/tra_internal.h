@@ -20,40 +20,49 @@ __host__ __device__ inline int coord_f(int32_t c) { return c >> 20; }
 __host__ __device__ inline int coord_x(int32_t c) { return (c >> 10) & 1023; }
 __host__ __device__ inline int coord_y(int32_t c) { return c & 1023; }
 
-constexpr int kBlockInfo = 8;  // f_min f_max x_min x_max y_min y_max n_valid 0
+// per block: f_min f_max x_min x_max y_min y_max n_video r_min r_max n_text
+constexpr int kBlockInfo = 10;
 constexpr int kMaxFrames = 64;
 constexpr int kMaxBlocks = 4096;
 constexpr int kSortChunk = 256;
 
 // Host-side tables of one shape (plan.cpp).
 struct HostTables {
-  int32_t N = 0, NB = 0, n_cap = 0;
-  std::vector<int32_t> perm;    // [N] tile-major position -> raster index
-  std::vector<int32_t> coord;   // [N] packed (f, x, y) of tile-major position
-  std::vector<int32_t> thr;     // [(n_cap + 1) * F]
+  int32_t N = 0, S = 0, NB = 0, n_cap = 0;  // video tokens, all tokens, blocks over S
+  std::vector<int32_t> perm;    // [S] tile-major position -> token index (text: N + t)
+  std::vector<int32_t> coord;   // [S] packed (f, x, y) of a video position, 0 for text
+  std::vector<int32_t> thr;     // [(n_cap + 1) * F] 2-D squared thresholds
+  std::vector<int32_t> thr1;    // [(n_cap + 1) * F] 1-D thresholds
   std::vector<int32_t> blocks;  // [NB * kBlockInfo]
 };
+
+// Phi^{-1}(p) of the standard normal in fp64, by bisection on Phi.
+double normal_quantile(double p);
 
 // Validates the config; on failure returns the status and fills `why`.
 tra_status validate_config(const tra_config* cfg, std::string* why);
 void build_host_tables(const tra_config& cfg, HostTables* t, bool with_perm_coord,
-                       bool with_thr, bool with_blocks);
+                       bool with_thr, bool with_thr1, bool with_blocks);
 
 }  // namespace tra
 
 struct tra_plan_s {
   tra_config cfg;
   int device = 0;
-  int32_t N = 0, NB = 0, n_cap = 0, rows = 0;
+  int32_t N = 0;   // video tokens F*H*W
+  int32_t S = 0;   // all tokens (video then text): the row length of every tensor
+  int32_t NB = 0, n_cap = 0, rows = 0;
+  double z_tau = 0.0;  // Phi^{-1}(tau), lognormal budget mapping
   int32_t* d_perm = nullptr;
   int32_t* d_coord = nullptr;
   int32_t* d_thr = nullptr;
+  int32_t* d_thr1 = nullptr;  // 1-D thresholds (TRA_DIST_1D plans only)
   int32_t* d_blocks = nullptr;
   int32_t* d_sort_ws = nullptr;  // counting-sort workspace of the row order
   int64_t sort_ws_elems = 0;
   int32_t sort_chunks = 0;
   // bf16 plans: K and V gathered into tile-major order, [batch*heads][NB*block][d],
-  // rows past N zero-filled, so the attention loop addresses tiles affinely.
+  // rows past S zero-filled, so the attention loop addresses tiles affinely.
   int32_t n_pad = 0;
   uint16_t* d_kt = nullptr;
   uint16_t* d_vt = nullptr;

@@ -60,6 +60,80 @@ def test_small_full_parity(name):
     assert report["near_integer_budgets"] == 0
 
 
+# Joint text-video workloads: video grid + text tokens (ragged and aligned video
+# lengths, so the mixed video/text block and a pure text block both occur).
+JOINT = {
+    "joint_bf16_d128": SMALL["ragged_bf16_d128"].replace(name="joint_bf16_d128", text_tokens=77),
+    "joint_bf16_d64": SMALL["ragged_bf16_d64"].replace(name="joint_bf16_d64", text_tokens=200),
+    "joint_aligned_bf16": SMALL["aligned_bf16"].replace(name="joint_aligned_bf16", text_tokens=128),
+    "joint_fp32_tiny": synth.workload("tiny").replace(name="joint_fp32_tiny", text_tokens=40),
+}
+
+
+def _full_check(run, report):
+    w = run.w
+    tabs = OracleTables(w)
+    tol = TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
+    for b in range(w.batch):
+        for h in range(w.heads):
+            check_head(run, tabs, b, h, np.arange(w.n_blocks), tol, report)
+    check_lists(run)
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128"])
+def test_lognormal_budget_parity(name):
+    """App. B lognormal mapping: budgets (fp64 on both sides, ties at an integer
+    allowed one apart), radii, masks and outputs against the oracle."""
+    _gpu()
+    run = Run(SMALL[name], budget="lognormal")
+    report = {}
+    _full_check(run, report)
+    log(f"{name} lognormal: rho={retained_fraction(run):.4f} {report}")
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128"])
+@pytest.mark.parametrize("rule", ["vote", "union"])
+def test_sequence_distance_parity(name, rule):
+    """Sequence-distance ablation (App. C.1): masks bit-exact, outputs within
+    tolerance, against the oracle's 1-D test."""
+    _gpu()
+    run = Run(SMALL[name], rule=rule, distance="1d")
+    report = {}
+    _full_check(run, report)
+    log(f"{name} 1d {rule}: rho={retained_fraction(run):.4f} {report}")
+
+
+@pytest.mark.parametrize("name", list(JOINT))
+def test_joint_text_video_parity(name):
+    """Joint text-video attention (Sec. 3.2): entropy over all S keys, text
+    tokens FULL, text blocks dense as rows and columns, outputs against the
+    oracle over the joint sequence."""
+    _gpu()
+    w = JOINT[name]
+    run = Run(w)
+    report = {}
+    _full_check(run, report)
+    mask = run.mask.cpu().numpy().astype(bool)
+    first_text = w.n_video // w.block
+    assert mask[:, :, first_text:, :].all() and mask[:, :, :, first_text:].all()
+    log(f"{name}: rho={retained_fraction(run):.4f} {report}")
+
+
+@pytest.mark.parametrize("name", ["joint_bf16_d128", "joint_fp32_tiny"])
+def test_joint_zero_radius(name):
+    """Video radii 0: the video part of the mask is block diagonal (vote), the
+    text part dense; every video query still sees every text key."""
+    _gpu()
+    w = JOINT[name]
+    run = Run(w, radius_override=0)
+    mask = run.mask.cpu().numpy().astype(bool)
+    first_text = w.n_video // w.block
+    vid = mask[:, :, :first_text, :first_text]
+    assert np.array_equal(vid, np.broadcast_to(np.eye(first_text, dtype=bool), vid.shape))
+    assert mask[:, :, first_text:, :].all() and mask[:, :, :, first_text:].all()
+    check_lists(run)
+
+
 def test_single_token_closed_form():
     """N = 1: the only key has p = 1, so H = 0, o = v, radius 0, mask [[1]]."""
     _gpu()

@@ -30,18 +30,27 @@ def test_library_exports_every_declared_symbol():
     assert "gfx950" in tra.tra_version()
 
 
-@pytest.mark.parametrize("name", ["tiny", "wan13b_480p", "wan14b_720p", "hunyuan_720p"])
+@pytest.mark.parametrize("name", ["tiny", "wan13b_480p", "wan14b_720p", "hunyuan_720p",
+                                  "hunyuan_joint_720p", "tiny_text"])
 def test_host_tables_match_oracle(name):
-    w = synth.workload(name)
+    w = synth.workload("tiny").replace(text_tokens=77) if name == "tiny_text" else synth.workload(name)
     cfg = tra.Config.from_workload(w)
-    perm, thr, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    perm, thr, thr1, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    N = w.n_video
     assert ncap == O.n_cap(w.height, w.width)
-    assert np.array_equal(perm, O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w))
+    assert np.array_equal(perm, O.joint_order(
+        O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w), w.text_tokens))
     assert np.array_equal(thr, O.threshold_table(ncap, w.frames, w.gamma))
+    assert np.array_equal(thr1, O.threshold_table_1d(ncap, w.frames, w.gamma))
     f, x, y = O.grid_coords(w.frames, w.height, w.width)
     for u, (lo, hi) in enumerate(O.block_bounds(w.n_tokens, w.block)):
         r = perm[lo:hi]
-        want = [f[r].min(), f[r].max(), x[r].min(), x[r].max(), y[r].min(), y[r].max(), hi - lo, 0]
+        rv, n_text = r[r < N], int((r >= N).sum())
+        if len(rv):
+            want = [f[rv].min(), f[rv].max(), x[rv].min(), x[rv].max(), y[rv].min(), y[rv].max(),
+                    len(rv), rv.min(), rv.max(), n_text]
+        else:
+            want = [w.frames, -1, w.height, -1, w.width, -1, 0, N, -1, n_text]
         assert list(blocks[u]) == want, u
 
 
@@ -51,6 +60,8 @@ def test_tiny_layout_sizes():
     cfg3 = tra.Config.from_workload(synth.workload("hunyuan_720p"))
     assert cfg3.n_tokens == 118800 and cfg3.n_blocks == 929
     assert cfg3.n_tokens - (cfg3.n_blocks - 1) * 128 == 16
+    cfg4 = tra.Config.from_workload(synth.workload("hunyuan_joint_720p"))
+    assert cfg4.n_video == 118800 and cfg4.n_tokens == 119056 and cfg4.n_blocks == 931
 
 
 @pytest.mark.parametrize("change,status", [
@@ -58,7 +69,9 @@ def test_tiny_layout_sizes():
     (dict(frames=0), 1), (dict(frames=65), 2), (dict(height=2000), 2),
     (dict(tau=1.0), 1), (dict(tau=0.0), 1), (dict(gamma=-0.1), 1),
     (dict(gamma=float("nan")), 1), (dict(tile_h=0), 1), (dict(dtype="fp16"), 1),
-    (dict(rule="maj"), 1), (dict(batch=0), 1),
+    (dict(rule="maj"), 1), (dict(batch=0), 1), (dict(budget="gamma"), 1),
+    (dict(distance="3d"), 1), (dict(text_tokens=-1), 1),
+    (dict(text_tokens=4096 * 128), 2),   # more than 4096 blocks
 ])
 def test_invalid_configs_rejected(change, status):
     base = dict(batch=1, heads=2, frames=3, height=8, width=16, head_dim=128)
@@ -72,13 +85,13 @@ def test_invalid_configs_rejected(change, status):
 def test_fp32_block64_accepted_host_side():
     cfg = tra.Config(batch=1, heads=1, frames=2, height=8, width=8, head_dim=64, block=64,
                      tile_h=8, tile_w=8, dtype="fp32")
-    perm, thr, blocks, ncap = tra.tra_plan_host_tables(cfg)
-    assert ncap == 98 and thr.shape == (99, 2) and blocks.shape == (2, 8)
+    perm, thr, thr1, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    assert ncap == 98 and thr.shape == (99, 2) and thr1.shape == (99, 2) and blocks.shape == (2, 10)
 
 
 def test_null_arguments_are_errors_not_crashes():
     L = tra.lib()
-    assert L.tra_plan_host_tables(None, None, None, None, None) == 1
+    assert L.tra_plan_host_tables(None, None, None, None, None, None) == 1
     assert L.tra_plan_create(None, None) == 1
     assert L.tra_entropy(None, None, None, None, None, None, None) == 1
     assert L.tra_budget_radius(None, None, None, None, None) == 1
