@@ -182,6 +182,114 @@ def density_sweep(tra, plan, w, q, k, v, dense_ms, targets, iters=3):
     return rows
 
 
+def _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters):
+    import torch
+    tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(iters):
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+        b_.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b_))
+    return float(np.mean(ts))
+
+
+def mask_variants(tra, w, q, k, v, H, dense_ms, iters=3, tag=""):
+    """The plan's budget-mapping and distance options on the headline inputs,
+    from the same entropies: the lognormal mapping (App. B) and the
+    sequence-distance ablation (App. C.1), each with its budget/radius + mask
+    time, retained fraction and sparse attention time."""
+    import torch
+    B, Ha, N, d = q.shape
+    dense_flops = 4.0 * d * N * N * B * Ha
+    out = {}
+    for name, kw in (("uniform_2d", {}), ("lognormal_2d", {"budget": "lognormal"}),
+                     ("uniform_1d", {"distance": "1d"})):
+        name = name + tag
+        plan = tra.Plan(tra.Config.from_workload(w, **kw))
+        NB = plan.n_blocks
+        dev = q.device
+        bud = torch.empty(B, Ha, N, dtype=torch.int32, device=dev)
+        rad = torch.empty_like(bud)
+        mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
+        cnt = torch.empty(B, Ha, NB, dtype=torch.int32, device=dev)
+        cols = torch.empty(B, Ha, NB, NB, dtype=torch.int32, device=dev)
+        o = torch.empty_like(q)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        tra.tra_budget_radius(plan, H, bud, rad)
+        e[1].record()
+        tra.tra_build_block_mask(plan, rad, mask, cnt, cols, None)
+        e[2].record()
+        torch.cuda.synchronize()
+        fl = executed_flops(mask.cpu().numpy(), N, w.block, d)
+        rho = fl / dense_flops
+        ms = _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters)
+        out[name] = {"budget_radius_ms": round(e[0].elapsed_time(e[1]), 4),
+                     "mask_ms": round(e[1].elapsed_time(e[2]), 4),
+                     "mean_budget_fraction": round(float(bud.double().mean()) / N, 5),
+                     "retained_fraction": round(rho, 5), "sparse_ms": round(ms, 4),
+                     "speedup_vs_dense": round(dense_ms / ms, 4),
+                     "eta_proportionality": round(rho * dense_ms / ms, 4)}
+        log(f"mask variant {name}: rho {rho:.4f} sparse {ms:.3f} ms")
+        del plan
+    return out
+
+
+def joint_driver(tra, w, iters=3):
+    """Joint text-video attention (Sec. 3.2) on a joint workload: entropy over
+    all S keys, budget/radius, mask (text blocks dense), sparse and dense."""
+    import torch
+
+    import synth
+    t0 = time.time()
+    q_np, k_np, v_np = synth.generate(w)
+    conv = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    q, k, v = conv(q_np), conv(k_np), conv(v_np)
+    del q_np, k_np, v_np
+    log(f"joint inputs generated in {time.time() - t0:.1f} s")
+    plan = tra.Plan(tra.Config.from_workload(w))
+    B, Ha, S, d = q.shape
+    NB = plan.n_blocks
+    dev = q.device
+    H = torch.empty(B, Ha, S, dtype=torch.float32, device=dev)
+    rad = torch.empty(B, Ha, S, dtype=torch.int32, device=dev)
+    mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
+    cnt = torch.empty(B, Ha, NB, dtype=torch.int32, device=dev)
+    cols = torch.empty(B, Ha, NB, NB, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    tra.tra_entropy(plan, q, k, None, None, H)   # warm-up
+    e[0].record()
+    tra.tra_entropy(plan, q, k, None, None, H)
+    e[1].record()
+    tra.tra_budget_radius(plan, H, None, rad)
+    e[2].record()
+    tra.tra_build_block_mask(plan, rad, mask, cnt, cols, None)
+    e[3].record()
+    tra.tra_dense_attention(plan, q, k, v, o)
+    e[4].record()
+    torch.cuda.synchronize()
+    dense_ms = e[3].elapsed_time(e[4])
+    fl = executed_flops(mask.cpu().numpy(), S, w.block, d)
+    dense_flops = 4.0 * d * S * S * B * Ha
+    ms = _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters)
+    res = {"workload": (f"{w.name}: {w.heads} heads, head_dim {d}, {w.frames}x{w.height}x{w.width} "
+                        f"video + {w.text_tokens} text = {S} tokens, gamma {w.gamma}"),
+           "entropy_ms": round(e[0].elapsed_time(e[1]), 4),
+           "budget_radius_ms": round(e[1].elapsed_time(e[2]), 4),
+           "mask_ms": round(e[2].elapsed_time(e[3]), 4),
+           "dense_ms": round(dense_ms, 4), "sparse_ms": round(ms, 4),
+           "retained_fraction": round(fl / dense_flops, 5),
+           "sparse_tflops": round(fl / (ms * 1e-3) / 1e12, 2),
+           "speedup_vs_dense": round(dense_ms / ms, 4)}
+    log(f"joint: rho {fl / dense_flops:.4f} sparse {ms:.3f} ms dense {dense_ms:.3f} ms")
+    return res
+
+
 def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100):
     """Warm-up reuse sequence: step 0 from the generator, later steps drift
     q, k <- q, k + 0.02 N(0,1) (fp32 masters, re-rounded).  Every `refresh`
@@ -277,6 +385,7 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the density sweep and the warm-up reuse sequence")
     ap.add_argument("--reuse-steps", type=int, default=50)
+    ap.add_argument("--no-joint", action="store_true", help="skip the joint text-video workload")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -445,6 +554,18 @@ def main():
     if not args.no_extras and w.dtype == "bf16":
         log("density sweep at the paper's retained fractions (uniform budgets)")
         out["density_sweep"] = density_sweep(tra, plan, w, q, k, v, dn, [0.09, 0.15, 0.19])
+        log("budget mapping and distance options")
+        tra.tra_entropy(plan, q, k, None, None, H)
+        out["mask_variants"] = mask_variants(tra, w, q, k, v, H, dn)
+        # density-matched: one constant entropy whose uniform 2-D mask keeps
+        # ~15 % (the sweep's budget), through each option
+        k15 = out["density_sweep"][1]["uniform_budget"]
+        H.fill_(float(np.log(k15 / w.tau)))
+        out["mask_variants"].update(mask_variants(tra, w, q, k, v, H, dn, tag=f"_at_H=ln({k15}/tau)"))
+        if not args.no_joint:
+            jw = synth.workload("hunyuan_joint_720p")
+            log(f"joint text-video attention on {jw.name}")
+            out["joint_text_video"] = joint_driver(tra, jw)
         rw = synth.workload("reuse_480p")
         log(f"warm-up reuse sequence ({args.reuse_steps} steps)")
         out["reuse_sequence"] = reuse_driver(tra, rw, steps=args.reuse_steps)
