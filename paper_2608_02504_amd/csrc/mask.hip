@@ -32,10 +32,12 @@ __device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
 
 // Distance of a token pair from its position difference: squared Euclidean
 // (x, y) for 2-D, |raster difference| (carried in the first component) for 1-D.
+// (Coordinate differences are below 1024 in magnitude, so 24-bit multiplies
+// are exact.)
 template <int DIST>
 __device__ __forceinline__ int metric(int da, int db) {
   if constexpr (DIST == TRA_DIST_1D) return abs(da);
-  else return da * da + db * db;
+  else return __mul24(da, da) + __mul24(db, db);
 }
 
 // Position of a packed coordinate in the metric's space.
@@ -77,6 +79,7 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
     return;
   }
   const int n_u = min(B, N - q0);
+  const int u_frames = binfo[(size_t)u * kBlockInfo + 1] - binfo[(size_t)u * kBlockInfo + 0] + 1;
 
   for (int qi = t; qi < B; qi += blockDim.x) {
     if (qi < n_u) {
@@ -115,7 +118,7 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
       const int xmin = DIST == TRA_DIST_1D ? bi[7] : bi[2], xmax = DIST == TRA_DIST_1D ? bi[8] : bi[3];
       const int ymin = DIST == TRA_DIST_1D ? 0 : bi[4], ymax = DIST == TRA_DIST_1D ? 0 : bi[5];
       uint64_t all_m[QPL], part_m[QPL];
-      int n_all = 0;
+      int n_all = 0, n_reach = 0;
       bool any_part = false;
 #pragma unroll
       for (int s = 0; s < QPL; ++s) {
@@ -134,6 +137,8 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
         part_m[s] = ballot(!none && !all);
         n_all += popc(all_m[s]);
         any_part |= part_m[s] != 0;
+        // partial queries whose disk over v's frames is more than a point
+        n_reach += popc(ballot(!none && !all && t_hi > 0));
       }
       if (RULE == TRA_MASK_VOTE && 3 * n_all > n_u) {
         keep = true;   // every column already has c_j >= n_all > n_u / 3
@@ -141,6 +146,13 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
         keep = true;
       } else if (!any_part) {
         // every column has c_j = n_all; under the vote, 3 n_all <= n_u here
+        keep = false;
+      } else if (RULE == TRA_MASK_VOTE && 3 * (n_all + u_frames + n_reach) <= n_u) {
+        // The vote needs a column with 3 c_j > n_u.  A key j is covered by the
+        // n_all queries, by partial queries with a positive threshold, and by
+        // partial queries whose threshold there is 0 -- those only at their own
+        // (x, y), at most one per frame of u.  So no column reaches n_u / 3 and
+        // the block is dropped, exactly as Alg. 1 decides.
         keep = false;
       } else {
         int kx[QPL], ky[QPL], kf[QPL], c[QPL];
@@ -153,20 +165,58 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
           position<DIST>(cc, H, W, &kx[s], &ky[s], &kf[s]);
           c[s] = n_all;
         }
+        if (fmax - fmin <= 1) {
+          // Block v spans at most two frames, so a query needs two thresholds
+          // here: ta for keys of frame fmin, tb for keys of frame fmax.  The
+          // partial queries are then walked with their data broadcast from
+          // registers (v_readlane), no LDS round trip per query.
+          int ta[QPL], tb[QPL];
+          bool kfirst[QPL];
 #pragma unroll
-        for (int s2 = 0; s2 < QPL; ++s2) {
-          uint64_t m = part_m[s2];
-          while (m) {
-            const int qi = __ffsll((unsigned long long)m) - 1 + 64 * s2;
-            m &= m - 1;
-            int px, py, pf;
-            position<DIST>(s_c[qi], H, W, &px, &py, &pf);
-            const int32_t* Tp = s_T + qi * F;
+          for (int s = 0; s < QPL; ++s) {
+            const int qi = lane + 64 * s;
+            ta[s] = s_T[qi * F + abs(qf[s] - fmin)];
+            tb[s] = s_T[qi * F + abs(qf[s] - fmax)];
+            kfirst[s] = kf[s] == fmin;
+          }
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) {
-              const int dx = px - kx[s], dy = py - ky[s];
-              const int dl = abs(pf - kf[s]);
-              c[s] += (metric<DIST>(dx, dy) <= Tp[dl]) ? 1 : 0;
+          for (int s2 = 0; s2 < QPL; ++s2) {
+            uint64_t m = part_m[s2];
+            while (m) {
+              const int l = __ffsll((unsigned long long)m) - 1;
+              m &= m - 1;
+              const int px = __builtin_amdgcn_readlane(qx[s2], l);
+              const int py = __builtin_amdgcn_readlane(qy[s2], l);
+              const int pa = __builtin_amdgcn_readlane(ta[s2], l);
+              const int pb = __builtin_amdgcn_readlane(tb[s2], l);
+#pragma unroll
+              for (int s = 0; s < QPL; ++s)
+                c[s] += (metric<DIST>(px - kx[s], py - ky[s]) <= (kfirst[s] ? pa : pb)) ? 1 : 0;
+              if (RULE == TRA_MASK_UNION) {
+                bool hit = false;
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) hit |= kvalid[s] && c[s] > 0;
+                if (ballot(hit) != 0) break;  // one covered key decides the union
+              }
+            }
+            if (RULE == TRA_MASK_UNION && m != 0) break;
+          }
+        } else {
+#pragma unroll
+          for (int s2 = 0; s2 < QPL; ++s2) {
+            uint64_t m = part_m[s2];
+            while (m) {
+              const int qi = __ffsll((unsigned long long)m) - 1 + 64 * s2;
+              m &= m - 1;
+              int px, py, pf;
+              position<DIST>(s_c[qi], H, W, &px, &py, &pf);
+              const int32_t* Tp = s_T + qi * F;
+#pragma unroll
+              for (int s = 0; s < QPL; ++s) {
+                const int dx = px - kx[s], dy = py - ky[s];
+                const int dl = abs(pf - kf[s]);
+                c[s] += (metric<DIST>(dx, dy) <= Tp[dl]) ? 1 : 0;
+              }
             }
           }
         }

@@ -134,6 +134,30 @@ def test_joint_zero_radius(name):
     check_lists(run)
 
 
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128",
+                                  "joint_bf16_d128"])
+@pytest.mark.parametrize("radius", [3, 40, 250])
+@pytest.mark.parametrize("rule,distance", [("vote", "2d"), ("union", "2d"), ("vote", "1d")])
+def test_mid_radius_masks_exact(name, radius, rule, distance):
+    """Radii where most block pairs are partially covered (the key-by-key path
+    of the mask builder): every mask row and list equals the oracle's Alg. 1.
+    (250 exceeds the tiny grid's n_cap = 98, where it must act as FULL.)"""
+    _gpu()
+    w = JOINT.get(name) or SMALL[name]
+    run = Run(w, rule=rule, distance=distance, radius_override=radius)
+    tabs = OracleTables(w)
+    n_full = run.rad.cpu().numpy()
+    # a radius above n_cap is documented to act as FULL
+    n_full = np.where(n_full > tabs.ncap, O.RADIUS_FULL, n_full)
+    mask = run.mask.cpu().numpy().astype(bool)
+    for b in range(w.batch):
+        for h in range(w.heads):
+            M_ref = O.block_mask_rows(n_full[b, h], tabs.perm, w.block, tabs.F, tabs.H, tabs.W,
+                                      w.gamma, list(range(w.n_blocks)), rule=rule, distance=distance)
+            assert np.array_equal(mask[b, h], M_ref), (b, h, np.nonzero((mask[b, h] != M_ref).any(1))[0][:5])
+    check_lists(run)
+
+
 def test_single_token_closed_form():
     """N = 1: the only key has p = 1, so H = 0, o = v, radius 0, mask [[1]]."""
     _gpu()
