@@ -41,7 +41,7 @@ __all__ = [
     "block_mask_rows", "masked_attention_rows", "retained_fraction",
     "top_tau_support", "analytic_radius", "token_budget_lognormal",
     "lognormal_top_mass", "normal_quantile", "normal_tail", "threshold_table_1d",
-    "within_radius_1d", "joint_order",
+    "within_radius_1d", "joint_order", "token_attention_rows",
 ]
 
 
@@ -424,6 +424,48 @@ def masked_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, return_lse=F
         keys = np.concatenate([perm[v * b: min((v + 1) * b, N)]
                                for v in np.nonzero(mask_rows[r])[0]])
         s = alpha * (qt[rows] @ kt[keys].T)
+        m = s.max(dim=1, keepdim=True).values
+        e = torch.exp(s - m)
+        z = e.sum(dim=1, keepdim=True)
+        o_out.append(((e / z) @ vt[keys]).numpy())
+        lse_out.append((m + torch.log(z))[:, 0].numpy())
+        rows_out.append(rows)
+    rows_out = np.concatenate(rows_out)
+    if return_lse:
+        return rows_out, np.concatenate(o_out), np.concatenate(lse_out)
+    return rows_out, np.concatenate(o_out)
+
+
+def token_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, n_tok, F: int, H: int, W: int,
+                         gamma: float, distance: str = "2d", return_lse=False):
+    """TRA attention at token level (Sec. 3.2, Eq. 16 with the bias B(M) of
+    Eq. tra_attention_final) inside the retained blocks: a query i of block u
+    attends, with one softmax, to the keys j of the key blocks v with
+    M[u, v] = 1 for which M_ij = 1 (Eq. 15, or the 1-D test; text keys always,
+    text queries to every such key), and to no other key.  With block rows from
+    the union rule every covered key lies in a retained block, so this is Eq. 16
+    over all keys.  n_tok: per-token squared radii (token order).
+
+    q, k, v: (S, d) token order.  Returns (rows, O) [and lse] for the queries of
+    ``blocks``."""
+    perm = np.asarray(perm, dtype=np.int64)
+    S = perm.shape[0]
+    N = F * H * W
+    qt, kt, vt = _t(q), _t(k), _t(v)
+    alpha = 1.0 / math.sqrt(qt.shape[1])
+    n_tok = np.asarray(n_tok)
+    rows_out, o_out, lse_out = [], [], []
+    for r, u in enumerate(blocks):
+        rows = perm[u * b: min((u + 1) * b, S)]
+        keys = np.concatenate([perm[v * b: min((v + 1) * b, S)]
+                               for v in np.nonzero(mask_rows[r])[0]])
+        video = rows < N
+        M = torch.ones(len(rows), len(keys), dtype=torch.bool)
+        if video.any():
+            M[torch.as_tensor(video)] = token_mask_rows(rows[video], n_tok[rows[video]], F, H, W, gamma,
+                                                        keys=keys, distance=distance)
+        s = alpha * (qt[rows] @ kt[keys].T)
+        s = torch.where(M, s, torch.tensor(-math.inf, dtype=torch.float64))
         m = s.max(dim=1, keepdim=True).values
         e = torch.exp(s - m)
         z = e.sum(dim=1, keepdim=True)

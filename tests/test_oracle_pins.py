@@ -542,3 +542,85 @@ def test_joint_all_blocks_kept_is_dense_over_s():
     rows, o = O.masked_attention_rows(q, k, v, perm, b, range(nb), np.ones((nb, nb), dtype=bool))
     want = O.dense_attention(q[rows], k, v)
     assert np.allclose(o, want, atol=1e-12)
+
+
+# ------------------------------------------------ token-level attention (Eq. 16)
+def _rand_qkv(S, d, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((S, d)) for _ in range(3))
+
+
+def test_token_attention_full_radius_is_block_attention():
+    """FULL radii keep every key of a retained block: token level = block level."""
+    F, H, W, b, d = 3, 8, 8, 64, 16
+    S = F * H * W
+    q, k, v = _rand_qkv(S, d, 21)
+    perm = O.tile_major_order(F, H, W, 8, 8)
+    nb = S // b
+    rng = np.random.default_rng(2)
+    mask = rng.random((nb, nb)) < 0.5
+    np.fill_diagonal(mask, True)
+    n = np.full(S, O.RADIUS_FULL)
+    r1, o1 = O.token_attention_rows(q, k, v, perm, b, range(nb), mask, n, F, H, W, 0.6)
+    r2, o2 = O.masked_attention_rows(q, k, v, perm, b, range(nb), mask)
+    assert np.array_equal(r1, r2) and np.allclose(o1, o2, atol=1e-13)
+
+
+@pytest.mark.parametrize("distance", ["2d", "1d"])
+def test_token_attention_on_union_lists_is_eq16_over_all_keys(distance):
+    """Union-rule block rows contain every covered key, so token-level attention
+    on them equals a softmax over {j : M_ij = 1} taken over ALL keys."""
+    F, H, W, b, d, gamma = 3, 8, 16, 64, 16, 0.6
+    S = F * H * W
+    q, k, v = _rand_qkv(S, d, 23)
+    perm = O.tile_major_order(F, H, W, 8, 8)
+    rng = np.random.default_rng(4)
+    n = rng.integers(0, 60, S)
+    nb = S // b
+    mask = O.block_mask_rows(n, perm, b, F, H, W, gamma, range(nb), rule="union", distance=distance)
+    rows, o = O.token_attention_rows(q, k, v, perm, b, range(nb), mask, n, F, H, W, gamma, distance)
+    M = O.token_mask_rows(rows, n[rows], F, H, W, gamma, distance=distance).numpy()
+    s = (q[rows] @ k.T) / math.sqrt(d)
+    s = np.where(M, s, -np.inf)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    assert np.allclose(o, p @ v, atol=1e-12)
+
+
+def test_token_attention_radius_zero_closed_form():
+    """Radius 0: query i sees exactly the keys at its own (x, y) in every frame
+    (thresholds are 0 for every delta), i.e. a softmax over F keys."""
+    F, H, W, b, d = 4, 8, 8, 64, 8
+    S = F * H * W
+    q, k, v = _rand_qkv(S, d, 25)
+    perm = O.tile_major_order(F, H, W, 8, 8)
+    nb = S // b
+    n = np.zeros(S, dtype=np.int64)
+    rows, o = O.token_attention_rows(q, k, v, perm, b, range(nb), np.ones((nb, nb), bool), n, F, H, W, 0.6)
+    for a, i in enumerate(rows[:40]):
+        same = np.arange(F) * H * W + i % (H * W)
+        s = q[i] @ k[same].T / math.sqrt(d)
+        p = np.exp(s - s.max())
+        p /= p.sum()
+        assert np.allclose(o[a], p @ v[same], atol=1e-12)
+
+
+def test_token_attention_joint_text_keys_visible():
+    """Joint sequence: text queries attend to every retained key, video queries
+    additionally to every text key."""
+    F, H, W, b, d, T = 2, 8, 8, 64, 8, 30
+    N, S = F * H * W, F * H * W + T
+    q, k, v = _rand_qkv(S, d, 27)
+    perm = O.joint_order(O.tile_major_order(F, H, W, 8, 8), T)
+    nb = -(-S // b)
+    n = np.concatenate([np.zeros(N, dtype=np.int64), np.full(T, O.RADIUS_FULL)])
+    rows, o = O.token_attention_rows(q, k, v, perm, b, range(nb), np.ones((nb, nb), bool), n, F, H, W, 0.6)
+    for a, i in enumerate(rows):
+        if i >= N:
+            keys = np.arange(S)
+        else:
+            keys = np.concatenate([np.arange(F) * H * W + i % (H * W), np.arange(N, S)])
+        s = q[i] @ k[keys].T / math.sqrt(d)
+        p = np.exp(s - s.max())
+        p /= p.sum()
+        assert np.allclose(o[a], p @ v[keys], atol=1e-12)
