@@ -167,8 +167,11 @@ const char* tra_version(void);
  * with the online-softmax identity
  * H = log Z - sum_j p_ij s_ij of App. C.2 (Alg. 2).
  * q, k: inputs.  v, o: both NULL (entropy only), or both non-NULL, in which
- * case o also receives dense attention softmax(q k^T / sqrt(d)) v, bitwise equal
- * to tra_dense_attention's output (the fused warm-up step of Alg. 2).
+ * case o also receives dense attention softmax(q k^T / sqrt(d)) v (the fused
+ * warm-up step of Alg. 2).  For bf16 plans the fused call runs its own kernel
+ * (the key blocks split over two groups of waves and merged), so its o and
+ * entropy agree with tra_dense_attention's output and with the entropy-only
+ * call up to fp32 rounding, not bit for bit; fp32 plans share one kernel.
  * entropy: fp32 [batch][heads][S] output. */
 tra_status tra_entropy(tra_plan plan, const void* q, const void* k, const void* v,
                        void* o, float* entropy, void* stream);

@@ -345,6 +345,169 @@ __device__ __forceinline__ void pv_step(f32x16& oacc, const lds_u8* __restrict__
   oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, __builtin_bit_cast(bf16x8, bw), oacc, 0, 0, 0);
 }
 
+// Row of the workgroup with index b when workgroups are dealt to the 8 XCDs
+// round-robin by index: each XCD gets a contiguous range of rows (same head,
+// neighbouring query blocks, largely the same key tiles), so its L2 serves
+// them together.  A bijection of [0, rows): XCD x holds rows / 8 + (x < rows % 8).
+__device__ __forceinline__ int xcd_row(int b, int rows) {
+  const int x = b & 7, k = b >> 3;
+  const int per = rows >> 3, rem = rows & 7;
+  return x * per + min(x, rem) + k;
+}
+
+// ------------------------------------------------------------ softmax and copy helpers
+// Row max of a score tile as a max3 tree (short dependency chains), folded into
+// the running state like tile_max.
+template <bool ENT>
+__device__ __forceinline__ float tile_max_tree(const f32x16 (&s)[4], float scale_log2, RowState& st) {
+  float m4[4];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    const float a = fmaxf(fmaxf(s[kt][0], s[kt][1]), s[kt][2]);
+    const float b = fmaxf(fmaxf(s[kt][3], s[kt][4]), s[kt][5]);
+    const float c = fmaxf(fmaxf(s[kt][6], s[kt][7]), s[kt][8]);
+    const float d = fmaxf(fmaxf(s[kt][9], s[kt][10]), s[kt][11]);
+    const float e = fmaxf(fmaxf(s[kt][12], s[kt][13]), s[kt][14]);
+    m4[kt] = fmaxf(fmaxf(fmaxf(a, b), fmaxf(c, d)), fmaxf(e, s[kt][15]));
+  }
+  float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
+  mx = max_halves(mx);
+  const float m_new = fmaxf(st.m, mx * scale_log2);
+  const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
+  if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
+  st.l *= sc;
+  st.m = m_new;
+  return sc;
+}
+
+// dma16 pinned between two steps of a computation: it is issued after `after`
+// has been computed and before `before` is next used (both pass through the
+// statement untouched), so the compiler keeps it at that point of the
+// instruction stream instead of hoisting it next to the other copies.
+template <int LDS_STEP>
+__device__ __forceinline__ void dma16_between(const void* sbase, uint32_t voff, uint32_t lds_base, float after,
+                                              float& before) {
+  asm volatile("s_add_u32 m0, %3, %4\n\tglobal_load_lds_dwordx4 %1, %2"
+               : "+v"(before)
+               : "v"(voff), "s"(sbase), "s"(lds_base), "i"(LDS_STEP), "v"(after)
+               : "memory", "m0", "scc");
+}
+
+// Copy steps [J, JEND) of a tile (4 KB each), pinned after `after` and before
+// `before` is next used.
+template <int J, int JEND>
+__device__ __forceinline__ void copies_after(float after, float& before, uint32_t lds, const uint8_t* src,
+                                             uint32_t off) {
+  if constexpr (J < JEND) {
+    dma16_between<J * 4096>(src + J * 4096, off, lds, after, before);
+    copies_after<J + 1, JEND>(after, before, lds, src, off);
+  }
+}
+
+// S^T = K Q^T for one tile with NC copy steps of `src` issued in between, one
+// after every (QK_STEPS / NC)-th k-step, pinned by the LDS-read order.
+template <int D, int NC>
+__device__ __forceinline__ void qk_tile_copies(f32x16 (&s)[4], const lds_u8* __restrict__ kbuf, uint32_t kbase,
+                                               const bf16x8 (&qf)[Geo<D>::QK_STEPS], uint32_t lds,
+                                               const uint8_t* src, uint32_t off) {
+  constexpr int KK = Geo<D>::QK_STEPS;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
+  kbase = opaque(kbase);
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const uint32_t o = chunk_off(kbase, kk);
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) qk_step<D>(s[kt], kbuf, o, qf, kt, kk);
+    if constexpr (NC > 0) {
+      if (kk % (KK / NC) == KK / NC - 1) {
+        switch (kk / (KK / NC)) {
+          case 0: dma16<0 * 4096>(src + 0 * 4096, off, lds); break;
+          case 1: dma16<1 * 4096>(src + 1 * 4096, off, lds); break;
+          case 2: dma16<2 * 4096>(src + 2 * 4096, off, lds); break;
+          case 3: dma16<3 * 4096>(src + 3 * 4096, off, lds); break;
+          case 4: dma16<4 * 4096>(src + 4 * 4096, off, lds); break;
+          case 5: dma16<5 * 4096>(src + 5 * 4096, off, lds); break;
+          case 6: dma16<6 * 4096>(src + 6 * 4096, off, lds); break;
+          default: dma16<7 * 4096>(src + 7 * 4096, off, lds); break;
+        }
+      }
+    }
+  }
+  sched_reads_ahead<4 * KK, 1, 4>();
+}
+
+// O^T += V^T P^T for one tile with NC copy steps of `src` issued in between,
+// one after every (8 / NC)-th k-step, pinned by the LDS-read order (a copy
+// statement is a memory barrier for the compiler).
+template <int D, int NC>
+__device__ __forceinline__ void pv_tile_copies(f32x16 (&oacc)[Geo<D>::D_TILES], const lds_u8* __restrict__ vbuf,
+                                               uint32_t vbase, const uint32_t (&pb)[32], uint32_t lds,
+                                               const uint8_t* src, uint32_t off) {
+  const uint32_t vb0 = opaque(vbase);
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) {
+    const uint32_t o = chunk_off(vb0, ks);
+#pragma unroll
+    for (int dt = 0; dt < Geo<D>::D_TILES; ++dt) pv_step<D>(oacc[dt], vbuf, o, pb, ks, dt);
+    if constexpr (NC > 0) {
+      if (ks % (8 / NC) == 8 / NC - 1) {
+        switch (ks / (8 / NC)) {
+          case 0: dma16<0 * 4096>(src + 0 * 4096, off, lds); break;
+          case 1: dma16<1 * 4096>(src + 1 * 4096, off, lds); break;
+          case 2: dma16<2 * 4096>(src + 2 * 4096, off, lds); break;
+          case 3: dma16<3 * 4096>(src + 3 * 4096, off, lds); break;
+          case 4: dma16<4 * 4096>(src + 4 * 4096, off, lds); break;
+          case 5: dma16<5 * 4096>(src + 5 * 4096, off, lds); break;
+          case 6: dma16<6 * 4096>(src + 6 * 4096, off, lds); break;
+          default: dma16<7 * 4096>(src + 7 * 4096, off, lds); break;
+        }
+      }
+    }
+  }
+  sched_reads_ahead<8 * Geo<D>::D_TILES, 1, 4>();
+}
+
+// Weights of score pairs [P, PEND) of a tile (pair P = 8 kt + e / 2):
+// w = 2^(s alpha log2e - m) into the bf16 pairs pb[P], w summed into lp[kt]
+// (and w x into ap[kt]), four independent chains.  NC tile-copy steps of
+// `src` (4 KB each) are issued in between, spread evenly over the pairs and
+// pinned there by data dependences: a burst of the four waves' copies would
+// stall each wave on the memory queue, spread out they drain while the
+// exponentials run.  C counts the copy steps issued so far.
+template <int D, bool PV, bool ENT, int P0, int PEND, int NC, int P = P0>
+__device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, float (&lp)[4], float (&ap)[4],
+                                          uint32_t* pb, uint32_t lds, const uint8_t* src, uint32_t off) {
+  if constexpr (P < PEND) {
+    constexpr int kt = P / 8, e = (P % 8) * 2;
+    const float x0 = fmaf(s[kt][e], c, -m);
+    const float x1 = fmaf(s[kt][e + 1], c, -m);
+    const float w0 = __builtin_amdgcn_exp2f(x0);
+    const float w1 = __builtin_amdgcn_exp2f(x1);
+    lp[kt] += w0 + w1;
+    if (ENT) ap[kt] = fmaf(w0, x0, fmaf(w1, x1, ap[kt]));
+    if (PV) pb[P] = pack_bf16x2(w0, w1);
+    // copies [C, C_NEXT) follow this pair: ceil(NC (pairs done) / pairs in range)
+    constexpr int C = ((P - P0) * NC + (PEND - P0) - 1) / (PEND - P0);
+    constexpr int C_NEXT = ((P + 1 - P0) * NC + (PEND - P0) - 1) / (PEND - P0);
+    if constexpr (C_NEXT > C) {
+      if constexpr (P + 1 < 32) {
+        constexpr int kt2 = (P + 1) / 8, e2 = ((P + 1) % 8) * 2;
+        float nxt = s[kt2][e2];
+        copies_after<C, C_NEXT>(w0, nxt, lds, src, off);
+        s[kt2][e2] = nxt;
+      } else {
+        float nxt = lp[kt];
+        copies_after<C, C_NEXT>(w0, nxt, lds, src, off);
+        lp[kt] = nxt;
+      }
+    }
+    exp_pairs<D, PV, ENT, P0, PEND, NC, P + 1>(s, c, m, lp, ap, pb, lds, src, off);
+  }
+}
+
 template <int D, bool SPARSE, bool PV, bool ENT, int OCC>
 __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
@@ -365,6 +528,9 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   if (SPARSE && order) {
     r = order[blockIdx.x];
     if (r < 0 || r >= rows) return;
+  }
+  else {
+    r = xcd_row(blockIdx.x, rows);
   }
   const int bh = r / NB, u = r - bh * NB;
   const int t = threadIdx.x, lane = t & 63;
@@ -512,12 +678,216 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   }
 }
 
+// ------------------------------------------------------------ fused entropy + dense output
+// The warm-up step's call (App. C.2, Alg. 2 with O): entropy and the dense
+// output in one pass.  Its per-wave state (scores, P, O, Q and the entropy
+// sum) does not fit the 128 registers a wave has when two of the 4-wave
+// workgroups above share a CU, so this kernel keeps two waves per SIMD a
+// different way, with matrix and vector work overlapped on purpose:
+//
+// One workgroup of 8 waves per query-block row, in two groups of 4 waves that
+// share the row's 128 queries and split its key tiles (group g takes key
+// blocks g, g + 2, ...); wave w4 of either group owns queries
+// [32 w4, 32 w4 + 32) with its own running state, and the two groups' states
+// (m, l, a, O) are merged at the end with the online-softmax rescaling.  Each
+// group alternates a matrix phase (PV of its previous tile, QK^T of the
+// current one) and a vector phase (softmax and entropy of the current tile,
+// O rescale), group 1 one phase behind group 0, every phase split by a mid
+// and a closing workgroup barrier.  So on every SIMD one wave keeps the matrix
+// core busy while the other runs its softmax.
+//
+//   matrix phase i:  PV(i-1) | mid | QK^T(i), copies of V^T(i) in between
+//   vector phase i:  copies of K(i+1) in between the row max and the first
+//                    half of the exponentials | mid | second half, O rescale
+// V^T(i) goes into the group's V buffer once PV(i-1) is done (mid barrier of
+// matrix phase i) and is waited for at the end of vector phase i; K(i+1)
+// goes into its K buffer once QK^T(i) is done (end of matrix phase i) and is
+// waited for before the mid barrier of matrix phase i+1, so each copy has
+// about one and a half phases to land.
+constexpr int kFusedThreads = 512;
+
+template <int D>
+__global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
+    const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ entropy,
+    const int32_t* __restrict__ perm, int N, int n_pad, int NB, int rows, float scale_log2) {
+  using G = Geo<D>;
+  constexpr int TILE = kBK * D * 2;
+  constexpr int GROUP_BYTES = 2 * TILE;  // K tile, then V^T tile
+  constexpr int KS = TileCopy<D>::STEPS;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * GROUP_BYTES];
+  __shared__ float smemState[3 * kBQ];  // group 1's (m, l, a) per query, for the merge
+
+  const int r = xcd_row(blockIdx.x, rows);
+  const int bh = r / NB, u = r - bh * NB;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int g = wave >> 2, w4 = wave & 3;
+  const int col = lane & 31, half = lane >> 5;
+  const size_t head_off = (size_t)bh * N * D;
+  constexpr size_t kTileBytes = (size_t)kBK * D * 2;
+  const uint8_t* Kb = (const uint8_t*)(ktile + (size_t)bh * n_pad * D);
+  const uint8_t* Vb = (const uint8_t*)(vtile + (size_t)bh * n_pad * D);
+  uint8_t* gbuf = smem + g * GROUP_BYTES;
+  const uint32_t k_lds = (uint32_t)(uintptr_t)gbuf + w4 * 1024;
+  const uint32_t v_lds = k_lds + TILE;
+  const uint32_t k_off = k_lane_off<D>(w4, lane);
+  const uint32_t v_off = vt_lane_off(w4, lane);
+  const lds_u8* kbuf = (const lds_u8*)gbuf;
+  const lds_u8* vbuf = (const lds_u8*)(gbuf + TILE);
+
+  const int qpos = u * kBQ + w4 * 32 + col;
+  const bool qvalid = qpos < N;
+  const int qrow = qvalid ? perm[qpos] : 0;
+  bf16x8 qf[G::QK_STEPS];
+  {
+    const uint4* src = (const uint4*)(q + head_off + (size_t)qrow * D);
+#pragma unroll
+    for (int kk = 0; kk < G::QK_STEPS; ++kk) {
+      uint4 x = qvalid ? src[2 * kk + half] : make_uint4(0, 0, 0, 0);
+      qf[kk] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+  const int krow = (col & ~15) | ((col & 15) ^ (((col >> 2) & 3) == 1 || ((col >> 2) & 3) == 2 ? 12 : 0));
+  const uint32_t kbase = krow * D * 2 + ((half ^ swz<G::CH>(krow)) << 4);
+  const uint32_t vbase = col * kBK * 2 + ((half ^ swz<16>(col)) << 4);
+
+  f32x16 oacc[G::D_TILES];
+#pragma unroll
+  for (int i = 0; i < G::D_TILES; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
+  RowState st{-INFINITY, 0.f, 0.f};
+  uint32_t pb[32];
+  f32x16 s[4];
+
+  // Group g's phases matrix 0, vector 0, ..., vector n-1, matrix n run in
+  // slots g, g + 1, ...; both groups count n_slots slots of two barriers each.
+  const int n_g = (NB - g + 1) >> 1;
+  const int n_half = (NB + 1) >> 1;
+  const int n_slots = (NB & 1) ? 2 * n_half + 1 : 2 * n_half + 2;
+
+  int b_cur = g;  // key block of this group's tile i: 2 i + g
+  if (n_g > 0) issue_tile<D>(k_lds, Kb + b_cur * kTileBytes, k_off);
+  wait_vm<0>();
+  lds_barrier();
+  if (g == 1) {  // group 1 idles in slot 0
+    lds_barrier();
+    lds_barrier();
+  }
+
+  for (int i = 0; i < n_g; ++i) {
+    const bool has_next = i + 1 < n_g;
+    const int b_nxt = b_cur + 2;
+    // ---- matrix phase i
+    if (i > 0) pv_tile_copies<D, 0>(oacc, vbuf, vbase, pb, v_lds, Vb, v_off);
+    wait_vm<0>();  // this wave's part of K(i) has landed
+    lds_barrier();
+    qk_tile_copies<D, KS>(s, kbuf, kbase, qf, v_lds, Vb + b_cur * kTileBytes, v_off);
+    lds_barrier();
+    // ---- vector phase i
+    if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
+    const float sc = tile_max_tree<true>(s, scale_log2, st);
+    float lp[4] = {0.f, 0.f, 0.f, 0.f}, ap[4] = {0.f, 0.f, 0.f, 0.f};
+    if (has_next)
+      exp_pairs<D, true, true, 0, 16, KS>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb + b_nxt * kTileBytes, k_off);
+    else
+      exp_pairs<D, true, true, 0, 16, 0>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb, k_off);
+    lds_barrier();
+    exp_pairs<D, true, true, 16, 32, 0>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb, k_off);
+    st.l += (lp[0] + lp[1]) + (lp[2] + lp[3]);
+    st.a += (ap[0] + ap[1]) + (ap[2] + ap[3]);
+    if (__ballot(sc != 1.0f) != 0) {
+#pragma unroll
+      for (int dt = 0; dt < G::D_TILES; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[dt][e] *= sc;
+    }
+    if (has_next) wait_vm<KS>();  // V^T(i) has landed; K(i+1) may still be in flight
+    else wait_vm<0>();
+    lds_barrier();
+    b_cur = b_nxt;
+  }
+  // ---- matrix phase n: PV of the last tile
+  if (n_g > 0) pv_tile_copies<D, 0>(oacc, vbuf, vbase, pb, v_lds, Vb, v_off);
+  lds_barrier();
+  lds_barrier();
+  for (int k = g + 2 * n_g + 1; k < n_slots; ++k) {
+    lds_barrier();
+    lds_barrier();
+  }
+
+  // ---- merge group 1 into group 0.  Every tile copy has completed (the last
+  // vector phase waits for all of them), so group 1's buffers take its O.
+  float l_tot = sum_halves(st.l);
+  float a_tot = sum_halves(st.a);
+  const int qi = w4 * 32 + col;
+  if (g == 1) {
+    float4* dst = (float4*)(smem + GROUP_BYTES);
+#pragma unroll
+    for (int j = 0; j < 4 * G::D_TILES; ++j)
+      dst[j * 256 + w4 * 64 + lane] = make_float4(oacc[j >> 2][4 * (j & 3)], oacc[j >> 2][4 * (j & 3) + 1],
+                                                  oacc[j >> 2][4 * (j & 3) + 2], oacc[j >> 2][4 * (j & 3) + 3]);
+    if (half == 0) {
+      smemState[qi] = st.m;
+      smemState[kBQ + qi] = l_tot;
+      smemState[2 * kBQ + qi] = a_tot;
+    }
+  }
+  lds_barrier();
+  if (g == 1) return;
+  {
+    const float m1 = smemState[qi], l1 = smemState[kBQ + qi], a1 = smemState[2 * kBQ + qi];
+    // a group state with l = 0 saw no key (m = -inf) and contributes nothing
+    const float m = l1 > 0.f ? (l_tot > 0.f ? fmaxf(st.m, m1) : m1) : st.m;
+    const float s0 = l_tot > 0.f ? __builtin_amdgcn_exp2f(st.m - m) : 0.f;
+    const float s1 = l1 > 0.f ? __builtin_amdgcn_exp2f(m1 - m) : 0.f;
+    const float e0 = l_tot > 0.f ? s0 * (a_tot + l_tot * (st.m - m)) : 0.f;
+    const float e1 = l1 > 0.f ? s1 * (a1 + l1 * (m1 - m)) : 0.f;
+    a_tot = e0 + e1;
+    l_tot = s0 * l_tot + s1 * l1;
+    const float4* src = (const float4*)(smem + GROUP_BYTES);
+#pragma unroll
+    for (int j = 0; j < 4 * G::D_TILES; ++j) {
+      const float4 x = src[j * 256 + w4 * 64 + lane];
+      f32x16& acc = oacc[j >> 2];
+      const int e = 4 * (j & 3);
+      acc[e] = s0 * acc[e] + s1 * x.x;
+      acc[e + 1] = s0 * acc[e + 1] + s1 * x.y;
+      acc[e + 2] = s0 * acc[e + 2] + s1 * x.z;
+      acc[e + 3] = s0 * acc[e + 3] + s1 * x.w;
+    }
+  }
+
+  if (!qvalid) return;
+  const size_t tok = (size_t)bh * N + qrow;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  uint16_t* dst = o + tok * D;
+#pragma unroll
+  for (int dt = 0; dt < G::D_TILES; ++dt)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int d0 = dt * 32 + 8 * gq + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(oacc[dt][4 * gq] * inv, oacc[dt][4 * gq + 1] * inv);
+      w.y = pack_bf16x2(oacc[dt][4 * gq + 2] * inv, oacc[dt][4 * gq + 3] * inv);
+      *(uint2*)(dst + d0) = w;
+    }
+  if (half == 0) entropy[tok] = 0.69314718055994531f * (__log2f(l_tot) - a_tot / l_tot);
+}
+
+template <int D>
+void launch_fused_entropy_output(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  hipLaunchKernelGGL((attn_fused_kernel<D>), dim3(p.rows), dim3(kFusedThreads), 0, s, (const uint16_t*)a.q,
+                     p.d_kt, p.d_vt, (uint16_t*)a.o, a.entropy, p.d_perm, p.S, p.n_pad, p.NB, p.rows,
+                     scale_log2);
+}
+
 template <int D, bool SPARSE, bool PV, bool ENT>
 void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
-  // the fused entropy + output variant needs more than the 256 VGPRs a wave
-  // gets at two workgroups per CU
-  constexpr int kOcc = (PV && ENT) ? 1 : 2;
+  constexpr int kOcc = 2;
   const size_t list_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
   hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), list_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
@@ -540,7 +910,7 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
     if (e != hipSuccess) return e;
   }
   if (a.sparse) launch_variant<D, true, true, false>(p, a, s);
-  else if (a.entropy && a.o) launch_variant<D, false, true, true>(p, a, s);
+  else if (a.entropy && a.o) launch_fused_entropy_output<D>(p, a, s);
   else if (a.entropy) launch_variant<D, false, false, true>(p, a, s);
   else launch_variant<D, false, true, false>(p, a, s);
   return hipGetLastError();

