@@ -162,39 +162,37 @@ def density_sweep(tra, plan, w, q, k, v, dense_ms, targets, iters=3):
         build(khat)
         h32 = float(np.float32(math.log(khat / w.tau)))
         khat = int(min(max(math.ceil(w.tau * math.exp(h32)), 1), N))   # the budget actually used
-        tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(iters):
-            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
-            b_.record()
-            torch.cuda.synchronize()
-            ts.append(a.elapsed_time(b_))
-        ms = float(np.mean(ts))
+        ms = _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters)
+        tok_ms = _time_call(lambda: tra.tra_token_attention(plan, q, k, v, rad, cnt, cols, None, o), iters)
         rows.append({"target": target, "uniform_budget": khat, "retained_fraction": round(rho, 5),
                      "sparse_ms": round(ms, 4), "tflops_executed": round(fl / (ms * 1e-3) / 1e12, 2),
                      "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                      "speedup_vs_dense": round(dense_ms / ms, 4),
-                     "eta_proportionality": round(rho * dense_ms / ms, 4)})
-        log(f"density {target}: K_hat {khat} rho {rho:.4f} sparse {ms:.3f} ms")
+                     "eta_proportionality": round(rho * dense_ms / ms, 4),
+                     "token_level_ms": round(tok_ms, 4),
+                     "token_level_vs_block": round(ms / tok_ms, 4)})
+        log(f"density {target}: K_hat {khat} rho {rho:.4f} sparse {ms:.3f} ms token-level {tok_ms:.3f} ms")
     return rows
 
 
-def _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters):
+def _time_call(fn, iters):
+    """Mean HIP-event time of fn() on the current stream, after one untimed call."""
     import torch
-    tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+    fn()
     torch.cuda.synchronize()
     ts = []
     for _ in range(iters):
         a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o)
+        fn()
         b_.record()
         torch.cuda.synchronize()
         ts.append(a.elapsed_time(b_))
     return float(np.mean(ts))
+
+
+def _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters):
+    return _time_call(lambda: tra.tra_sparse_attention(plan, q, k, v, cnt, cols, None, o), iters)
 
 
 def mask_variants(tra, w, q, k, v, H, dense_ms, iters=3, tag=""):
@@ -490,6 +488,11 @@ def main():
         dense_ms.append(a.elapsed_time(b_))
         fused_ms.append(b_.elapsed_time(c))
 
+    # token-level TRA attention (the token mask inside the same retained blocks)
+    log("token-level attention on the step's radii and lists")
+    token_ms = _time_call(lambda: tra.tra_token_attention(plan, q, k, v, rad, cnt, cols, None, o_sp),
+                          max(1, args.dense_iters))
+
     mask_np = mask.cpu().numpy()
     flops = executed_flops(mask_np, N, w.block, d)
     dense_flops = 4.0 * d * N * N * B * Ha
@@ -536,6 +539,7 @@ def main():
         "stage_ms": {n_: round(v_, 4) for n_, v_ in stage_ms.items()},
         "stage_min_ms": {n_: round(v_, 4) for n_, v_ in stage_min.items()},
         "entropy_plus_dense_output_ms": round(float(np.mean(fused_ms)), 4),
+        "token_level_ms": round(token_ms, 4),
         "entropy_gbs": round(ent_bytes / (stage_ms["entropy"] * 1e-3) / 1e9, 1),
         "entropy_tflops": round(2.0 * d * N * N * B * Ha / (stage_ms["entropy"] * 1e-3) / 1e12, 2),
         "budget_radius_gbs": round(rad_bytes / (stage_ms["budget_radius"] * 1e-3) / 1e9, 1),

@@ -16,6 +16,8 @@
  *                         per-row lists of retained key blocks.
  *   tra_sparse_attention  block-sparse attention over the retained blocks
  *                         (Sec. 3.2, Eq. 16, executed at block granularity).
+ *   tra_token_attention   the same over the retained blocks with the token
+ *                         mask of Eq. 15 applied inside them (Eq. 16 exactly).
  *   tra_dense_attention   dense attention (Sec. 2.1, Eq. 1), the baseline.
  *
  * Tensors and layout
@@ -53,7 +55,8 @@
  * until the stream has drained.  The plan owns its small device tables, a
  * sort workspace and, for bf16 plans, a key/value workspace of
  * 2 x batch x heads x NB x 128 x head_dim x 2 bytes into which every
- * attention call (tra_entropy, tra_sparse_attention, tra_dense_attention)
+ * attention call (tra_entropy, tra_sparse_attention, tra_token_attention,
+ * tra_dense_attention)
  * first rewrites K and V in tile-major order (V transposed per block).  Calls
  * that share a plan must therefore not overlap in time on different streams
  * when they use a workspace (those three calls on bf16 plans, and
@@ -217,6 +220,30 @@ tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t
 tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
                                 const void* v, const int32_t* cnt, const int32_t* cols,
                                 const int32_t* order, void* o, float* lse, void* stream);
+
+/* Token-level TRA attention inside the retained blocks (Sec. 3.2, Eq. 16 with
+ * the -inf bias of the token mask, Eq. 15; App. D names the block-granular
+ * execution's redundant in-block work as the method's main limitation).  A
+ * video query i of block u takes one softmax over the keys j of the key
+ * blocks cols[r][0..cnt[r]) that its radius covers -- the same integer test as
+ * tra_build_block_mask: (x_i-x_j)^2 + (y_i-y_j)^2 <= thr[n_i][|f_i-f_j|], or
+ * for TRA_DIST_1D |i - j| <= thr1[n_i][|f_i-f_j|] -- plus every text key of
+ * those blocks; a text query attends to every key of its retained blocks.
+ * With lists from the union rule every covered key lies in a listed block,
+ * so this is Eq. 16 over all keys.  radius_sq: int32 [batch][heads][S] input
+ * (raster order, as written by tra_budget_radius; values above n_cap mean the
+ * full radius, negative ones 0).  q, k, v, cnt, cols, order, o, lse as for
+ * tra_sparse_attention; a query's own key is always covered, so a query of a
+ * row that lists its own block never has an empty softmax; a query that
+ * covers no listed key gets o = 0, lse = -inf.  Whole 128-key tiles that none
+ * of a wave's 32 queries covers are skipped.  bf16 plans need every threshold
+ * below 65536 (n_cap <= 65535 for 2-D, floor(pi/2 n_cap) <= 65535 for 1-D)
+ * and at least one block of video tokens per frame (H*W >= block), else
+ * TRA_ERR_UNSUPPORTED. */
+tra_status tra_token_attention(tra_plan plan, const void* q, const void* k, const void* v,
+                               const int32_t* radius_sq, const int32_t* cnt,
+                               const int32_t* cols, const int32_t* order, void* o,
+                               float* lse, void* stream);
 
 /* Dense attention o_i = sum_j softmax_j(q_i k_j / sqrt(d)) v_j (Eq. 1), the
  * baseline the sparse call is measured against.  lse as above, or NULL. */

@@ -6,7 +6,7 @@ torch is used for device memory and streams.  The functions keep the C names:
 
     tra_plan_create / tra_plan_destroy / tra_plan_dims / tra_plan_host_tables
     tra_entropy / tra_budget_radius / tra_build_block_mask
-    tra_sparse_attention / tra_dense_attention
+    tra_sparse_attention / tra_token_attention / tra_dense_attention
 
 There is no fallback: if libtra.so is missing or fails to load, every call
 raises.
@@ -23,7 +23,8 @@ __all__ = [
     "LIB_PATH", "TRA_RADIUS_FULL", "TraError", "Config", "Plan", "lib", "library_loaded",
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
     "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
-    "tra_sparse_attention", "tra_dense_attention", "tra_version", "EXPORTED_SYMBOLS",
+    "tra_sparse_attention", "tra_token_attention", "tra_dense_attention", "tra_version",
+    "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtra.so")
@@ -38,7 +39,7 @@ _DIST = {"2d": TRA_DIST_2D, "1d": TRA_DIST_1D}
 EXPORTED_SYMBOLS = (
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
     "tra_last_error", "tra_version", "tra_entropy", "tra_budget_radius",
-    "tra_build_block_mask", "tra_sparse_attention", "tra_dense_attention",
+    "tra_build_block_mask", "tra_sparse_attention", "tra_token_attention", "tra_dense_attention",
 )
 
 _STATUS = {0: "TRA_OK", 1: "TRA_ERR_INVALID_ARG", 2: "TRA_ERR_UNSUPPORTED",
@@ -131,10 +132,11 @@ def lib() -> ctypes.CDLL:
     L.tra_budget_radius.argtypes = [P, V, V, V, V]
     L.tra_build_block_mask.argtypes = [P, V, V, V, V, V, V]
     L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V]
+    L.tra_token_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, V]
     L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V]
     for name in ("tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
                  "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
-                 "tra_sparse_attention", "tra_dense_attention"):
+                 "tra_sparse_attention", "tra_token_attention", "tra_dense_attention"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -298,6 +300,22 @@ def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, str
     _check(lib().tra_sparse_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(cnt),
                                       _ptr(cols), _ptr(order), _ptr(o), _ptr(lse),
                                       _stream(stream)))
+
+
+def tra_token_attention(plan: Plan, q, k, v, radius_sq, cnt, cols, order, o, lse=None, stream=None):
+    import torch
+    tok, per, rowsh, sq = _shapes(plan)
+    dt = _qkv_dtype(plan)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _want(t, tok, dt, n)
+    _want(radius_sq, per, torch.int32, "radius_sq")
+    _want(cnt, rowsh, torch.int32, "cnt")
+    _want(cols, sq, torch.int32, "cols")
+    _want(order, (plan.rows,), torch.int32, "order")
+    _want(lse, per, torch.float32, "lse")
+    _check(lib().tra_token_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(radius_sq),
+                                     _ptr(cnt), _ptr(cols), _ptr(order), _ptr(o), _ptr(lse),
+                                     _stream(stream)))
 
 
 def tra_dense_attention(plan: Plan, q, k, v, o, lse=None, stream=None):

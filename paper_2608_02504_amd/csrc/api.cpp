@@ -110,6 +110,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_sort_ws);
   (void)hipFree(p->d_kt);
   (void)hipFree(p->d_vt);
+  (void)hipFree(p->d_kinfo);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -134,7 +135,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
 
     tra::HostTables t;
     const bool one_d = cfg->distance == TRA_DIST_1D;
-    tra::build_host_tables(*cfg, &t, true, true, one_d, true);
+    tra::build_host_tables(*cfg, &t, true, true, one_d, true, cfg->dtype == TRA_BF16);
 
     tra_plan p = new tra_plan_s();
     p->cfg = *cfg;
@@ -149,6 +150,8 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
     // chunk histograms over keys 0..NB, plus one total slot
     p->sort_ws_elems = (int64_t)(t.NB + 1) * p->sort_chunks + 1;
     p->n_pad = t.NB * cfg->block;
+    // the largest threshold: thr[n][0] = n, thr1[n][0] = floor(pi/2 n), at n = n_cap
+    p->thr_max = one_d ? t.thr1[(size_t)t.n_cap * cfg->frames] : t.n_cap;
 
     auto upload = [&](int32_t** dst, const std::vector<int32_t>& src) -> hipError_t {
       hipError_t err = hipMalloc((void**)dst, src.size() * sizeof(int32_t));
@@ -167,7 +170,8 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
     if (cfg->dtype == TRA_BF16) {
       const size_t bytes = (size_t)cfg->batch * cfg->heads * p->n_pad * cfg->head_dim * sizeof(uint16_t);
       if ((e = hipMalloc((void**)&p->d_kt, bytes)) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_vt, bytes)) != hipSuccess) {
+          (e = hipMalloc((void**)&p->d_vt, bytes)) != hipSuccess ||
+          (e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess) {
         tra_plan_destroy(p);
         return fail(TRA_ERR_ALLOC, std::string("plan K/V workspace: ") + hipGetErrorString(e));
       }
@@ -250,6 +254,29 @@ tra_status tra_sparse_attention(tra_plan p, const void* q, const void* k, const 
   TRA_TRY(check_aligned4(lse, "lse", true));
   tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true};
   return run_attention(p, a, stream, "tra_sparse_attention launch");
+}
+
+tra_status tra_token_attention(tra_plan p, const void* q, const void* k, const void* v,
+                               const int32_t* radius_sq, const int32_t* cnt, const int32_t* cols,
+                               const int32_t* order, void* o, float* lse, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_tensor(q, "q"));
+  TRA_TRY(check_tensor(k, "k"));
+  TRA_TRY(check_tensor(v, "v"));
+  TRA_TRY(check_tensor(o, "o"));
+  TRA_TRY(check_aligned4(radius_sq, "radius_sq", false));
+  TRA_TRY(check_aligned4(cnt, "cnt", false));
+  TRA_TRY(check_aligned4(cols, "cols", false));
+  TRA_TRY(check_aligned4(order, "order", true));
+  TRA_TRY(check_aligned4(lse, "lse", true));
+  if (p->cfg.dtype == TRA_BF16) {
+    if (p->thr_max > 65535)
+      return fail(TRA_ERR_UNSUPPORTED, "token attention on bf16 plans needs every threshold below 65536");
+    if (p->cfg.height * p->cfg.width < p->cfg.block)
+      return fail(TRA_ERR_UNSUPPORTED, "token attention on bf16 plans needs height * width >= block");
+  }
+  tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true, radius_sq};
+  return run_attention(p, a, stream, "tra_token_attention launch");
 }
 
 tra_status tra_dense_attention(tra_plan p, const void* q, const void* k, const void* v,

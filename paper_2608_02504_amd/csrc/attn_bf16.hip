@@ -37,6 +37,7 @@
 //   On a max increase m -> m': l <- 2^{m-m'} l, a <- 2^{m-m'} (a + l (m - m')).
 //   H = ln(l) - ln(2) a / l  (nats)  == log Z - sum_j p_j s_j (App. C.2).
 //   Each lane keeps l and a over its own keys; the halves are added at the end.
+#include <climits>
 #include <cmath>
 
 #include "tra_internal.h"
@@ -297,6 +298,14 @@ struct RowState {
   float m, l, a;  // running max (log2 units), sum of weights, entropy sum
 };
 
+// Floor of the running max (log2 units), far below any real score and far
+// above the masked ones (-1e30 times the scale): a tile whose keys are all
+// masked for a query then leaves m at the floor and gives its masked keys
+// weight 2^(-1e29) = 0.  Without it m would be the masked value itself, and
+// s * scale - m, formed by one fma from the exact product, would leave the
+// product's rounding error (~1e22) instead of 0 -- an infinite weight.
+constexpr float kMaxFloor = -1.0e20f;
+
 // Max of a score tile folded into the running state; returns the factor that
 // rescales everything accumulated so far (0 on the first tile).
 template <bool ENT>
@@ -307,7 +316,7 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
   mx = max_halves(mx);
-  const float m_new = fmaxf(st.m, mx * scale_log2);
+  const float m_new = fmaxf(fmaxf(st.m, mx * scale_log2), kMaxFloor);
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;
@@ -345,6 +354,71 @@ __device__ __forceinline__ void pv_step(f32x16& oacc, const lds_u8* __restrict__
   oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, __builtin_bit_cast(bf16x8, bw), oacc, 0, 0, 0);
 }
 
+// ------------------------------------------------------------ token mask inside a tile
+// Inputs of the token-level variant (Eq. 15 inside the listed blocks).
+struct TokArgs {
+  const int32_t* radius_sq;  // [B*Ha][S] per-token squared radii, raster order
+  const int32_t* thr;        // [(n_cap + 1) * F] thresholds (2-D or 1-D per the plan)
+  const int32_t* kinfo;      // [NB][kKeyInfo] key distance words, then frames
+  const int32_t* binfo;      // [NB][kBlockInfo] block boxes
+  const int32_t* coord;      // [S] packed (f, x, y) per tile-major position
+  int Nv, F, n_cap;
+};
+
+typedef short short2_t __attribute__((ext_vector_type(2)));
+typedef int int4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int4v lds_read_i4(const lds_u8* base, uint32_t off) {
+  return *(const __attribute__((address_space(3))) int4v*)(base + off);
+}
+
+// Distance between a query and a key from their distance words: 2-D squared
+// Euclidean distance of the packed (x, y) (packed 16-bit subtract, then a
+// 16-bit dot product), or |i - j| of raster indices for the 1-D ablation.
+template <int TOK>
+__device__ __forceinline__ int token_metric(int qw, int kw) {
+  if constexpr (TOK == 2) {
+    return abs(qw - kw);
+  } else {
+    const short2_t d = __builtin_bit_cast(short2_t, qw) - __builtin_bit_cast(short2_t, kw);
+    return __builtin_amdgcn_sdot2(d, d, 0, false);
+  }
+}
+
+// Token mask of one score tile for this lane's query: element e of sub-tile
+// kt is key 32 kt + 16 (e / 8) + 8 half + e % 8 of the block; it keeps its
+// score iff the query covers the key (distance <= the query's threshold for
+// the key's frame: t_lo for the block's first frame, t_hi for its second) or
+// the key is a text token, else gets the same large negative score as the
+// ragged tail.  kinfo: the block's 128 key words (distance word, second-frame
+// flag at bit 15 for 2-D / 30 for 1-D, text flag at bit 31).  One code path for
+// every block: a second, single-frame specialisation would not fit the
+// kernel's registers alongside it.
+template <int TOK>
+__device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restrict__ kinfo, int half,
+                                           int qw, int t_lo, int t_hi) {
+  const uint32_t neg = __float_as_uint(-1.0e30f);
+  constexpr int kFrameBit = TOK == 2 ? 30 : 15;
+  constexpr uint32_t kWordMask = TOK == 2 ? 0x3FFFFFFFu : 0x7FFF7FFFu;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+#pragma unroll
+      for (int h4 = 0; h4 < 2; ++h4) {
+        const int k0 = kt * 32 + 16 * g + 8 * half + 4 * h4;  // 4 consecutive keys
+        const int4v w = lds_read_i4(kinfo, 4 * k0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int dist = token_metric<TOK>(qw, (int)((uint32_t)w[j] & kWordMask));
+          const bool keep = w[j] < 0 || dist <= (((w[j] >> kFrameBit) & 1) ? t_hi : t_lo);
+          const int e = 8 * g + 4 * h4 + j;
+          s[kt][e] = keep ? s[kt][e] : __uint_as_float(neg);
+        }
+      }
+    }
+}
+
 // Row of the workgroup with index b when workgroups are dealt to the 8 XCDs
 // round-robin by index: each XCD gets a contiguous range of rows (same head,
 // neighbouring query blocks, largely the same key tiles), so its L2 serves
@@ -372,7 +446,7 @@ __device__ __forceinline__ float tile_max_tree(const f32x16 (&s)[4], float scale
   }
   float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
   mx = max_halves(mx);
-  const float m_new = fmaxf(st.m, mx * scale_log2);
+  const float m_new = fmaxf(fmaxf(st.m, mx * scale_log2), kMaxFloor);
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;
@@ -508,21 +582,28 @@ __device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, floa
   }
 }
 
-template <int D, bool SPARSE, bool PV, bool ENT, int OCC>
+// TOK (sparse only): 0 block granular; 1 token mask with the 2-D distance,
+// 2 with the 1-D sequence distance (Eq. 15 inside the listed blocks).
+template <int D, bool SPARSE, bool PV, bool ENT, int OCC, int TOK = 0>
 __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
     const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ lse,
     float* __restrict__ entropy, const int32_t* __restrict__ perm, const int32_t* __restrict__ cnt,
     const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N, int n_pad, int NB,
-    int rows, float scale_log2) {
+    int rows, float scale_log2, TokArgs tk) {
   using G = Geo<D>;
   constexpr int TILE = kBK * D * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t smemK[TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t smemV[PV ? TILE : 16];
+  // token variant: key words of the current and the next tile (a 1 KB copy
+  // each, of which the first 512 B are the tile's)
+  __shared__ __attribute__((aligned(16))) uint8_t smemKinfo[TOK ? 2 * 1024 : 16];
   // the row's key-block list (dynamic LDS, NB entries for the sparse variant),
   // read once so that the tile loop issues no global loads of its own (a wait
-  // for one would also drain the tiles in flight)
+  // for one would also drain the tiles in flight); the token variant then
+  // keeps each query's thresholds by frame distance, [128][F] uint16
   extern __shared__ int32_t smemCols[];
+  uint16_t* thrq = (uint16_t*)(smemCols + ((NB + 3) & ~3));
 
   int r = blockIdx.x;
   if (SPARSE && order) {
@@ -561,6 +642,23 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   if constexpr (SPARSE) {
     const int32_t* colp = cols + (size_t)r * NB;
     for (int j = t; j < count; j += kThreads) smemCols[j] = colp[j];
+  }
+  // token variant: this lane's query as a distance word and frame; a text
+  // query or a full radius covers every key (thresholds then INT_MAX)
+  [[maybe_unused]] int tq_word = 0, tq_f = 0;
+  [[maybe_unused]] bool tq_all = true;
+  const int qi = wave * 32 + col;
+  if constexpr (TOK != 0) {
+    if (qvalid && qpos < tk.Nv) {
+      int n = tk.radius_sq[(size_t)bh * N + qrow];
+      tq_all = n > tk.n_cap;
+      n = max(n, 0);
+      const int32_t c = tk.coord[qpos];
+      tq_f = coord_f(c);
+      tq_word = TOK == 2 ? qrow : (coord_x(c) | (coord_y(c) << 16));
+      if (!tq_all)
+        for (int d = half; d < tk.F; d += 2) thrq[qi * tk.F + d] = (uint16_t)tk.thr[(size_t)n * tk.F + d];
+    }
   }
   // retire the Q and list loads before any tile load is in flight, so that no
   // compiler wait for them lands inside the tile loop (it would also drain the
@@ -602,55 +700,117 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
     for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
   RowState st{-INFINITY, 0.f, 0.f};
 
+  // token variant: wave 0 copies each tile's key info (1 KB) right after its
+  // K steps, into the buffer of the tile's parity, so "K landed" covers it
+  [[maybe_unused]] const uint32_t kinfo_lds = (uint32_t)(uintptr_t)smemKinfo;
+  auto issue_kinfo = [&](int b, int parity) {
+    if constexpr (TOK != 0) {
+      if (wave == 0) dma16<0>((const uint8_t*)(tk.kinfo + (size_t)b * kKeyInfo), lane * 16, kinfo_lds + parity * 1024);
+    }
+  };
   int b_cur;
   int i = next_valid(0, &b_cur);
+  int parity = 0;
   if (i < count) {
+    b_cur = __builtin_amdgcn_readfirstlane(b_cur);
     issue_tile<D>(k_lds, Kb + b_cur * kTileBytes, k_off);
+    issue_kinfo(b_cur, 0);
     if (PV) issue_tile<D>(v_lds, Vb + b_cur * kTileBytes, v_off);
     for (;;) {
       int b_nxt;
       const int i_nxt = next_valid(i + 1, &b_nxt);
       const bool has_next = i_nxt < count;
+      b_nxt = __builtin_amdgcn_readfirstlane(b_nxt);
       wait_vm<PV ? TileCopy<D>::STEPS : 0>();  // K_i landed (V_i may still be in flight)
       lds_barrier();
-      f32x16 s[4];
-      qk_tile<D>(s, (const lds_u8*)smemK, kbase, qf);
-      lds_barrier();  // every wave is done with K_i
-      if (has_next) issue_tile<D>(k_lds, Kb + b_nxt * kTileBytes, k_off);
-      if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
-      const float sc = tile_max<ENT>(s, scale_log2, st);
-      uint32_t pb[32];
-      float lsum = 0.f, asum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
+      // token variant: classify this lane's query against the block's box
+      // ("none": no key of the block covered; "all": every video key covered)
+      // with its thresholds for the block's nearest and farthest frames; a
+      // wave none of whose queries covers a key skips the tile's matrix work,
+      // a wave all of whose queries cover every key skips the key test
+      bool wave_skip = false, wave_test = false;
+      int t_lo = INT_MAX, t_hi = INT_MAX;
+      if constexpr (TOK != 0) {
+        const int32_t* bi = tk.binfo + (size_t)b_cur * kBlockInfo;
+        const int fmin = bi[0], fmax = bi[1], n_video = bi[6], n_text = bi[9];
+        bool none = !qvalid, all = true;
+        if (qvalid && n_video > 0 && !tq_all) {
+          t_lo = thrq[qi * tk.F + abs(tq_f - fmin)];
+          t_hi = thrq[qi * tk.F + abs(tq_f - fmax)];
+          int dmin, dmax;
+          if constexpr (TOK == 2) {
+            const int rmin = bi[7], rmax = bi[8];
+            dmin = max(0, max(rmin - tq_word, tq_word - rmax));
+            dmax = max(tq_word - rmin, rmax - tq_word);
+          } else {
+            const int qx = tq_word & 0xFFFF, qy = tq_word >> 16;
+            const int dxn = max(0, max(bi[2] - qx, qx - bi[3])), dyn = max(0, max(bi[4] - qy, qy - bi[5]));
+            const int dxf = max(qx - bi[2], bi[3] - qx), dyf = max(qy - bi[4], bi[5] - qy);
+            dmin = dxn * dxn + dyn * dyn;
+            dmax = dxf * dxf + dyf * dyf;
+          }
+          none = n_text == 0 && dmin > max(t_lo, t_hi);
+          all = dmax <= min(t_lo, t_hi);
+        }
+        wave_skip = __ballot(!none) == 0;
+        wave_test = __ballot(!all) != 0;
       }
-      st.l += lsum;
-      if (ENT) st.a += asum;
+      f32x16 s[4];
+      if (!wave_skip) qk_tile<D>(s, (const lds_u8*)smemK, kbase, qf);
+      lds_barrier();  // every wave is done with K_i
+      if (has_next) {
+        issue_tile<D>(k_lds, Kb + b_nxt * kTileBytes, k_off);
+        issue_kinfo(b_nxt, parity ^ 1);
+      }
+      float sc = 1.f;
+      uint32_t pb[32];
+      if (!wave_skip) {
+        if constexpr (TOK != 0) {
+          if (wave_test) {
+            const lds_u8* ki = (const lds_u8*)smemKinfo + parity * 1024;
+            token_mask<TOK>(s, ki, half, tq_word, t_lo, t_hi);
+          }
+        }
+        if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
+        sc = tile_max<ENT>(s, scale_log2, st);
+        float lsum = 0.f, asum = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
+        }
+        st.l += lsum;
+        if (ENT) st.a += asum;
+      }
       if constexpr (PV) {
-        if (has_next) wait_vm<TileCopy<D>::STEPS>();  // V_i landed (K_{i+1} may still be in flight)
+        // V_i landed (K_{i+1} -- and for wave 0 of the token variant its key
+        // info -- may still be in flight)
+        if (has_next && TOK != 0 && wave == 0) wait_vm<TileCopy<D>::STEPS + 1>();
+        else if (has_next) wait_vm<TileCopy<D>::STEPS>();
         else wait_vm<0>();
         lds_barrier();
-        if (__ballot(sc != 1.0f) != 0) {
+        if (!wave_skip) {
+          if (__ballot(sc != 1.0f) != 0) {
 #pragma unroll
-          for (int dt = 0; dt < G::D_TILES; ++dt)
+            for (int dt = 0; dt < G::D_TILES; ++dt)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) oacc[dt][e] *= sc;
+              for (int e = 0; e < 16; ++e) oacc[dt][e] *= sc;
+          }
+          const uint32_t vb0 = opaque(vbase);
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) {
+            const uint32_t off = chunk_off(vb0, ks);
+#pragma unroll
+            for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], (const lds_u8*)smemV, off, pb, ks, dt);
+          }
+          sched_reads_ahead<8 * G::D_TILES, 1, 4>();
         }
-        const uint32_t vb0 = opaque(vbase);
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          const uint32_t off = chunk_off(vb0, ks);
-#pragma unroll
-          for (int dt = 0; dt < G::D_TILES; ++dt) pv_step<D>(oacc[dt], (const lds_u8*)smemV, off, pb, ks, dt);
-        }
-        sched_reads_ahead<8 * G::D_TILES, 1, 4>();
         lds_barrier();  // every wave is done with V_i
         if (has_next) issue_tile<D>(v_lds, Vb + b_nxt * kTileBytes, v_off);
       }
       if (!has_next) break;
       i = i_nxt;
       b_cur = b_nxt;
+      parity ^= 1;
     }
   }
 
@@ -884,14 +1044,16 @@ void launch_fused_entropy_output(const tra_plan_s& p, const AttnArgs& a, hipStre
                      scale_log2);
 }
 
-template <int D, bool SPARSE, bool PV, bool ENT>
+template <int D, bool SPARSE, bool PV, bool ENT, int TOK = 0>
 void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
-  constexpr int kOcc = 2;
-  const size_t list_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, kOcc>), dim3(p.rows), dim3(kThreads), list_bytes, s,
+  size_t lds_bytes = SPARSE ? (size_t)((p.NB + 3) & ~3) * sizeof(int32_t) : 0;
+  if (TOK != 0) lds_bytes += (size_t)kBQ * p.cfg.frames * sizeof(uint16_t);
+  const TokArgs tk{a.radius_sq, p.cfg.distance == TRA_DIST_1D ? p.d_thr1 : p.d_thr, p.d_kinfo, p.d_blocks,
+                   p.d_coord, p.N, p.cfg.frames, p.n_cap};
+  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>), dim3(p.rows), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
-                     a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2);
+                     a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2, tk);
 }
 
 template <int D>
@@ -909,7 +1071,9 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (a.sparse) launch_variant<D, true, true, false>(p, a, s);
+  if (a.sparse && a.radius_sq && p.cfg.distance == TRA_DIST_1D) launch_variant<D, true, true, false, 2>(p, a, s);
+  else if (a.sparse && a.radius_sq) launch_variant<D, true, true, false, 1>(p, a, s);
+  else if (a.sparse) launch_variant<D, true, true, false>(p, a, s);
   else if (a.entropy && a.o) launch_fused_entropy_output<D>(p, a, s);
   else if (a.entropy) launch_variant<D, false, false, true>(p, a, s);
   else launch_variant<D, false, true, false>(p, a, s);

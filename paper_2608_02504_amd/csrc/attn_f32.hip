@@ -1,6 +1,9 @@
-// fp32 attention family (dense, block-sparse, fused entropy) for fp32
-// workloads.  Scalar fp32 arithmetic with one thread per query row; the bf16
-// path is the MFMA kernel.  One workgroup per query-block row.
+// fp32 attention family (dense, block-sparse, token-level sparse, fused
+// entropy) for fp32 workloads.  Scalar fp32 arithmetic with one thread per
+// query row; the bf16 path is the MFMA kernel.  One workgroup per query-block
+// row.  The token-level variant (Eq. 16 with the token mask of Eq. 15 inside
+// the listed blocks) tests every (query, key) pair with the plan's integer
+// thresholds, as the block-mask kernel does.
 //
 // Online softmax with the entropy accumulator of Alg. 2 (App. C.2), kept
 // relative to the running maximum m: per row l = sum_j e^{s_j - m} and
@@ -28,14 +31,36 @@ struct F32Params {
   const int32_t* order;
   int N, NB, rows;
   float alpha;
+  // token-level attention only
+  const int32_t* radius_sq;
+  const int32_t* thr;  // [(n_cap + 1) * F], 2-D or 1-D thresholds per the plan
+  int Nv, F, H, W, n_cap;
 };
+
+// Does video query i (radius n, raster index) cover video key j (raster
+// index)?  DIST as in the block mask: 2-D squared distance or 1-D |i - j|.
+template <int DIST>
+__device__ __forceinline__ bool covers(const F32Params& P, int i, int n, int j) {
+  const int HW = P.H * P.W;
+  const int fi = i / HW, fj = j / HW;
+  int dist;
+  if (DIST == TRA_DIST_1D) {
+    dist = abs(i - j);
+  } else {
+    const int dx = (i / P.W) % P.H - (j / P.W) % P.H, dy = i % P.W - j % P.W;
+    dist = dx * dx + dy * dy;
+  }
+  return dist <= P.thr[(size_t)n * P.F + abs(fi - fj)];
+}
 
 constexpr int kSub = 32;  // keys staged in LDS at a time
 
-template <int D, int B, bool SPARSE, bool PV, bool ENT>
+// TOK: 0 block-granular, 1 token mask with 2-D distance, 2 with 1-D distance.
+template <int D, int B, bool SPARSE, bool PV, bool ENT, int TOK = 0>
 __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
   __shared__ float sK[kSub][D + 1];
   __shared__ float sV[PV ? kSub : 1][PV ? D + 1 : 1];
+  __shared__ int sPos[kSub];  // raster index of each staged key
 
   int r = blockIdx.x;
   if (SPARSE && P.order) {
@@ -56,6 +81,14 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
 #pragma unroll
   for (int d = 0; d < (PV ? D : 1); ++d) acc[d] = 0.f;
   float m = -INFINITY, l = 0.f, a = 0.f;
+  // token mask: a text query (or a FULL radius) covers every key
+  int n_i = 0;
+  bool all_keys = true;
+  if (TOK && qvalid && qpos < P.Nv) {
+    n_i = P.radius_sq[(size_t)bh * P.N + qrow];
+    all_keys = n_i > P.n_cap;
+    n_i = max(n_i, 0);
+  }
 
   const int count = SPARSE ? min(max(P.cnt[r], 0), P.NB) : P.NB;
   for (int c = 0; c < count; ++c) {
@@ -76,6 +109,7 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
         sK[j][d] = kv;
         if (PV) sV[j][d] = vv;
       }
+      if (TOK && t < kSub) sPos[t] = t < ns ? P.perm[vb * B + j0 + t] : 0;
       __syncthreads();
       float s[kSub];
       float mc = -INFINITY;
@@ -84,9 +118,13 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
         float dot = 0.f;
 #pragma unroll
         for (int d = 0; d < D; ++d) dot = fmaf(qr[d], sK[j][d], dot);
-        s[j] = j < ns ? dot * P.alpha : -INFINITY;
+        bool keep = j < ns;
+        if (TOK && keep && !all_keys && sPos[j] < P.Nv)
+          keep = covers<TOK == 2 ? TRA_DIST_1D : TRA_DIST_2D>(P, qrow, n_i, sPos[j]);
+        s[j] = keep ? dot * P.alpha : -INFINITY;
         mc = fmaxf(mc, s[j]);
       }
+      if (TOK && mc == -INFINITY) continue;  // no covered key here: nothing to add
       const float mn = fmaxf(m, mc);
       const float sc = expf(m - mn);  // 0 on the first sub-tile (m = -inf)
       if (ENT) a = l > 0.f ? sc * (a + l * (m - mn)) : 0.f;
@@ -121,11 +159,17 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
 
 template <int D, int B>
 hipError_t launch_f32_db(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+  const bool one_d = p.cfg.distance == TRA_DIST_1D;
   F32Params P{(const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.o, a.lse,
               a.entropy, p.d_perm, a.cnt, a.cols, a.order, p.S, p.NB, p.rows,
-              1.0f / sqrtf((float)D)};
+              1.0f / sqrtf((float)D), a.radius_sq, one_d ? p.d_thr1 : p.d_thr, p.N,
+              p.cfg.frames, p.cfg.height, p.cfg.width, p.n_cap};
   const dim3 grid(p.rows), block(B);
-  if (a.sparse)
+  if (a.sparse && a.radius_sq && one_d)
+    hipLaunchKernelGGL((attn_f32_kernel<D, B, true, true, false, 2>), grid, block, 0, s, P);
+  else if (a.sparse && a.radius_sq)
+    hipLaunchKernelGGL((attn_f32_kernel<D, B, true, true, false, 1>), grid, block, 0, s, P);
+  else if (a.sparse)
     hipLaunchKernelGGL((attn_f32_kernel<D, B, true, true, false>), grid, block, 0, s, P);
   else if (a.entropy && a.o)
     hipLaunchKernelGGL((attn_f32_kernel<D, B, false, true, true>), grid, block, 0, s, P);

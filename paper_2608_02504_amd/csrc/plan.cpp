@@ -66,7 +66,7 @@ double normal_quantile(double p) {
 }
 
 void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
-                       bool with_thr, bool with_thr1, bool with_blocks) {
+                       bool with_thr, bool with_thr1, bool with_blocks, bool with_kinfo) {
   const int F = c.frames, H = c.height, W = c.width, b = c.block;
   t->N = F * H * W;
   t->S = t->N + c.text_tokens;
@@ -74,7 +74,7 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
   t->n_cap = (H - 1) * (H - 1) + (W - 1) * (W - 1);
 
   std::vector<int32_t> perm;
-  if (with_perm_coord || with_blocks) {
+  if (with_perm_coord || with_blocks || with_kinfo) {
     // One frame's tile-major order, then offset per frame; text tokens last.
     std::vector<int32_t> frame;
     frame.reserve((size_t)H * W);
@@ -131,6 +131,32 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
       o[0] = fmin; o[1] = fmax; o[2] = xmin; o[3] = xmax; o[4] = ymin; o[5] = ymax;
       o[6] = std::max(0, hi - lo); o[7] = rmin; o[8] = rmax;
       o[9] = hi_all - std::max(lo, t->N) > 0 ? hi_all - std::max(lo, t->N) : 0;
+    }
+  }
+  if (with_kinfo) {
+    // key side of the token mask: one word per key of every block (and one
+    // zero block after the last, so a 1 KB copy of the last block stays in
+    // bounds).  2-D: x | y << 16, 1-D: the raster index; plus a flag bit
+    // (bit 15 for 2-D, bit 30 for 1-D) when the key lies in the block's second
+    // frame (a block of at most H*W tokens spans at most two), and bit 31 for
+    // a text key.  Positions past S stay 0 (the ragged tail is masked apart).
+    const bool one_d = c.distance == TRA_DIST_1D;
+    t->kinfo.assign((size_t)(t->NB + 1) * kKeyInfo, 0);
+    for (int u = 0; u < t->NB; ++u) {
+      const int f0 = u * b < t->N ? perm[(size_t)u * b] / (H * W) : 0;
+      for (int j = 0; j < b; ++j) {
+        const int p = u * b + j;
+        uint32_t word = 0;
+        if (p < t->N) {
+          const int i = perm[p];
+          const bool second = i / (H * W) != f0;
+          word = one_d ? (uint32_t)i | (second ? 1u << 30 : 0u)
+                       : (uint32_t)((i / W) % H) | ((uint32_t)(i % W) << 16) | (second ? 1u << 15 : 0u);
+        } else if (p < t->S) {
+          word = 1u << 31;
+        }
+        t->kinfo[(size_t)u * kKeyInfo + j] = (int32_t)word;
+      }
     }
   }
   if (with_perm_coord) t->perm = std::move(perm);

@@ -22,6 +22,7 @@ __host__ __device__ inline int coord_y(int32_t c) { return c & 1023; }
 
 // per block: f_min f_max x_min x_max y_min y_max n_video r_min r_max n_text
 constexpr int kBlockInfo = 10;
+constexpr int kKeyInfo = 128;  // ints per key block in the key-info table
 constexpr int kMaxFrames = 64;
 constexpr int kMaxBlocks = 4096;
 constexpr int kSortChunk = 256;
@@ -34,6 +35,7 @@ struct HostTables {
   std::vector<int32_t> thr;     // [(n_cap + 1) * F] 2-D squared thresholds
   std::vector<int32_t> thr1;    // [(n_cap + 1) * F] 1-D thresholds
   std::vector<int32_t> blocks;  // [NB * kBlockInfo]
+  std::vector<int32_t> kinfo;   // [(NB + 1) * kKeyInfo]
 };
 
 // Phi^{-1}(p) of the standard normal in fp64, by bisection on Phi.
@@ -42,7 +44,7 @@ double normal_quantile(double p);
 // Validates the config; on failure returns the status and fills `why`.
 tra_status validate_config(const tra_config* cfg, std::string* why);
 void build_host_tables(const tra_config& cfg, HostTables* t, bool with_perm_coord,
-                       bool with_thr, bool with_thr1, bool with_blocks);
+                       bool with_thr, bool with_thr1, bool with_blocks, bool with_kinfo = false);
 
 }  // namespace tra
 
@@ -66,6 +68,11 @@ struct tra_plan_s {
   int32_t n_pad = 0;
   uint16_t* d_kt = nullptr;
   uint16_t* d_vt = nullptr;
+  // bf16 plans: per key block, 128 distance words (2-D: x | y << 16; 1-D: the
+  // raster index) with a second-frame flag and a text flag, [NB + 1][128],
+  // the key side of the token mask inside a tile.
+  int32_t* d_kinfo = nullptr;
+  int32_t thr_max = 0;  // largest entry of the plan's threshold table
 };
 
 namespace tra {
@@ -85,6 +92,7 @@ struct AttnArgs {
   const int32_t* cols;   // sparse only
   const int32_t* order;  // sparse only, may be null
   bool sparse;
+  const int32_t* radius_sq = nullptr;  // token-level attention (sparse) only
 };
 hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_f32(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);

@@ -1,0 +1,157 @@
+"""GPU parity of token-level TRA attention (tra_token_attention: Eq. 16 with
+the token mask of Eq. 15 applied inside the retained blocks) against the
+oracle's token_attention_rows, through the C ABI.  Radii and block lists come
+from the GPU path (they are checked bit-exact against the oracle elsewhere);
+the oracle then takes the same radii and rows.  Bars as for block-sparse
+attention: 2e-2 max-abs for bf16 I/O, 1e-5 for fp32."""
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from _pipeline import TOL_O_BF16, TOL_O_FP32, OracleTables, Run, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+W = {
+    "tiny": synth.workload("tiny"),
+    "ragged_fp32_d128_b128": synth.Workload("ragged_fp32_d128_b128", 1, 2, 128, "fp32", 3, 7, 19, 128,
+                                            0.25, 4.0, 0.6, seed=77, tile_h=8, tile_w=16),
+    "ragged_bf16_d128": synth.Workload("ragged_bf16_d128", 1, 2, 128, "bf16", 4, 13, 37, 128,
+                                       0.25, 4.0, 0.6, seed=78, tile_h=8, tile_w=16),
+    "ragged_bf16_d64": synth.Workload("ragged_bf16_d64", 2, 2, 64, "bf16", 3, 11, 29, 128,
+                                      0.1, 8.0, 0.95, seed=79, tile_h=8, tile_w=16),
+    "aligned_bf16": synth.Workload("aligned_bf16", 1, 2, 128, "bf16", 5, 16, 32, 128,
+                                   0.25, 4.0, 0.6, seed=80, tile_h=8, tile_w=16),
+    "fp32_b64_d128": synth.Workload("fp32_b64_d128", 1, 1, 128, "fp32", 2, 9, 11, 64,
+                                    0.25, 4.0, 0.6, seed=82, tile_h=8, tile_w=8),
+}
+W["joint_bf16_d128"] = W["ragged_bf16_d128"].replace(name="joint_bf16_d128", text_tokens=77)
+W["joint_fp32"] = W["ragged_fp32_d128_b128"].replace(name="joint_fp32", text_tokens=50)
+
+
+def _token_call(run, cnt=None, cols=None, order=None):
+    import torch
+    import paper_2608_02504_amd as tra
+    o = torch.empty_like(run.q)
+    lse = torch.empty_like(run.lse_sp)
+    tra.tra_token_attention(run.plan, run.q, run.k, run.v, run.rad,
+                            run.cnt if cnt is None else cnt, run.cols if cols is None else cols,
+                            order, o, lse)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def _check_against_oracle(run, o, lse, tol):
+    """Every query row of every (batch, head) against token_attention_rows."""
+    w = run.w
+    tabs = OracleTables(w)
+    NB = run.plan.n_blocks
+    worst = 0.0
+    for b in range(w.batch):
+        for h in range(w.heads):
+            q, k, v = (synth.to_f64(a[b, h], w.dtype) for a in (run.q_np, run.k_np, run.v_np))
+            M = run.mask[b, h].cpu().numpy().astype(bool)
+            n_tok = run.rad[b, h].cpu().numpy()
+            rows, o_ref, lse_ref = O.token_attention_rows(
+                q, k, v, tabs.perm, w.block, list(range(NB)), M, n_tok, tabs.F, tabs.H, tabs.W,
+                w.gamma, distance=run.cfg.distance, return_lse=True)
+            o_gpu = o[b, h].double().cpu().numpy()[rows]
+            err = np.abs(o_gpu - o_ref).max()
+            assert err <= tol, f"token attention max-abs {err:.3e} (b={b}, h={h})"
+            lse_gpu = lse[b, h].double().cpu().numpy()[rows]
+            assert np.abs(lse_gpu - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "token lse"
+            worst = max(worst, float(err))
+    return worst
+
+
+@pytest.mark.parametrize("name", list(W))
+@pytest.mark.parametrize("rule", ["vote", "union"])
+def test_token_attention_parity(name, rule):
+    _gpu()
+    w = W[name]
+    run = Run(w, rule=rule)
+    o, lse = _token_call(run, order=run.order)
+    tol = TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
+    err = _check_against_oracle(run, o, lse, tol)
+    log(f"{name} {rule}: token attention max-abs {err:.2e}")
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny"])
+@pytest.mark.parametrize("radius", [0, 3, 40])
+def test_token_attention_forced_radii_1d_and_2d(name, radius):
+    """Fixed radii for every video query, both distances: masks with many
+    partially covered tiles, tiles no query of a wave covers, and (radius 0)
+    rows whose only key is the query itself."""
+    _gpu()
+    w = W[name]
+    tol = TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
+    for distance in ("2d", "1d"):
+        run = Run(w, rule="union", radius_override=radius, distance=distance)
+        o, lse = _token_call(run)
+        _check_against_oracle(run, o, lse, tol)
+        if radius == 0 and distance == "1d":
+            # |i - j| <= 0 keeps only the query's own key: o_i = v_i exactly
+            v = run.v[..., :w.n_video, :]
+            assert np.array_equal(o[..., :w.n_video, :].float().cpu().numpy(), v.float().cpu().numpy())
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny", "joint_bf16_d128"])
+def test_token_full_radius_equals_sparse_bitwise(name):
+    """Every radius FULL: every query covers every key of its retained blocks,
+    so token-level attention is the block-sparse call, bit for bit."""
+    _gpu()
+    import torch
+    run = Run(W[name], radius_override=2 ** 31 - 1)
+    o, lse = _token_call(run)
+    assert torch.equal(o, run.O_sp)
+    assert torch.equal(lse, run.lse_sp)
+
+
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny"])
+def test_token_out_of_range_column_ids_are_skipped(name):
+    """Lists padded with -1 / NB entries give the same output as clean lists."""
+    _gpu()
+    import torch
+    run = Run(W[name], radius_override=40)
+    NB = run.plan.n_blocks
+    cnt, cols = run.cnt.cpu().numpy(), run.cols.cpu().numpy()
+    cnt2, cols2 = np.zeros_like(cnt), np.full_like(cols, -1)
+    for idx in np.ndindex(cnt.shape):
+        valid = cols[idx][:cnt[idx]].tolist()
+        out = []
+        for c in valid:
+            out += [-1, c]
+        out = (out + [NB])[:NB]
+        kept = [c for c in out if 0 <= c < NB]
+        cnt2[idx], cols2[idx][:len(out)] = len(out), out
+        cnt[idx], cols[idx][:len(kept)] = len(kept), kept
+    dev = run.q.device
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    ref = _token_call(run, cnt=t(cnt), cols=t(cols))
+    got = _token_call(run, cnt=t(cnt2), cols=t(cols2))
+    assert torch.equal(got[0], ref[0]) and torch.equal(got[1], ref[1])
+
+
+def test_token_unsupported_shapes_are_rejected():
+    """bf16 token attention needs thresholds below 65536 and H*W >= block."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    for cfg in (tra.Config(batch=1, heads=1, frames=1, height=300, width=300, head_dim=64),
+                tra.Config(batch=1, heads=1, frames=3, height=8, width=8, head_dim=64)):
+        plan = tra.Plan(cfg)
+        S, NB = cfg.n_tokens, plan.n_blocks
+        x = torch.zeros(1, 1, S, 64, dtype=torch.bfloat16, device="cuda")
+        rad = torch.zeros(1, 1, S, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, 1, NB, dtype=torch.int32, device="cuda")
+        cols = torch.zeros(1, 1, NB, NB, dtype=torch.int32, device="cuda")
+        with pytest.raises(tra.TraError, match="UNSUPPORTED"):
+            tra.tra_token_attention(plan, x, x, x, rad, cnt, cols, None, torch.empty_like(x))
