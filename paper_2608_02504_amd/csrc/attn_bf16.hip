@@ -306,6 +306,19 @@ struct RowState {
 // product's rounding error (~1e22) instead of 0 -- an infinite weight.
 constexpr float kMaxFloor = -1.0e20f;
 
+// Lazy rescaling: the exponent reference m of a query moves only when a tile's
+// max exceeds it by more than kMaxSlack (log2 units).  Weights then stay below
+// 2^kMaxSlack = 256 (fine for the fp32 sums and the bf16 probabilities), the
+// normalisation by l at the end is unchanged, and the O rescale -- and with it
+// most of the max bookkeeping -- runs on the first tiles of a row only.
+constexpr float kMaxSlack = 8.0f;
+
+// New exponent reference of one query from its tile max (log2 units).
+__device__ __forceinline__ float next_reference(float m, float tile_max_scaled) {
+  const float m_new = tile_max_scaled > m + kMaxSlack ? tile_max_scaled : m;
+  return fmaxf(m_new, kMaxFloor);
+}
+
 // Max of a score tile folded into the running state; returns the factor that
 // rescales everything accumulated so far (0 on the first tile).
 template <bool ENT>
@@ -316,7 +329,7 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
   mx = max_halves(mx);
-  const float m_new = fmaxf(fmaxf(st.m, mx * scale_log2), kMaxFloor);
+  const float m_new = next_reference(st.m, mx * scale_log2);
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;
@@ -446,7 +459,7 @@ __device__ __forceinline__ float tile_max_tree(const f32x16 (&s)[4], float scale
   }
   float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
   mx = max_halves(mx);
-  const float m_new = fmaxf(fmaxf(st.m, mx * scale_log2), kMaxFloor);
+  const float m_new = next_reference(st.m, mx * scale_log2);
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;

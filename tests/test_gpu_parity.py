@@ -293,6 +293,7 @@ def _sampled(name, heads=None):
         if heads is not None and h not in heads:
             continue
         check_head(run, tabs, b, h, blocks, TOL_O_BF16, report)
+        log(f"{name}: batch {b} head {h} checked")  # progress of the long CPU-side check
     rho = retained_fraction(run)
     log(f"{name}: rho={rho:.4f} sampled {BLOCKS_PER_HEAD} blocks/head {report}")
     assert report["near_integer_budgets"] == 0
