@@ -1,6 +1,9 @@
 // bf16 attention family on gfx950 matrix cores: dense attention (Eq. 1),
-// block-sparse TRA attention (Eq. 16 at block granularity) and the fused
-// online-softmax entropy pass (App. C.2, Alg. 2), all from one template.
+// block-sparse TRA attention (Eq. 16 at block granularity), its token-level
+// form (the token mask of Eq. 15 inside the retained blocks) and the
+// online-softmax entropy pass (App. C.2, Alg. 2), all from one 4-wave
+// template; plus an 8-wave split-key kernel for the entropy pass fused with
+// the dense output (at the end of the file).
 //
 // Layout pre-pass
 //   K and V are first gathered into tile-major order (Sec. 3.3: tokens of a
