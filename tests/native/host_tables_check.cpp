@@ -1,0 +1,135 @@
+// Host-side check of the plan's table builder (plan.cpp), built by the CPU
+// test suite with AddressSanitizer and UndefinedBehaviorSanitizer: every
+// workload shape and a set of edge shapes (text tokens, 1-D distance, block
+// 64, a single token, clipped tiles) are validated and built, and the tables'
+// invariants checked; invalid configurations must be rejected.  Exit status 0
+// and no sanitizer report mean pass.
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "tra_internal.h"
+
+namespace {
+
+int failures = 0;
+
+void expect(bool ok, const char* what, int cfg) {
+  if (!ok) {
+    std::printf("FAIL config %d: %s\n", cfg, what);
+    ++failures;
+  }
+}
+
+tra_config make(int F, int H, int W, int d, int b, int th, int tw, int text, int dtype, int dist) {
+  tra_config c{};
+  c.batch = 1; c.heads = 2; c.frames = F; c.height = H; c.width = W; c.head_dim = d; c.block = b;
+  c.tile_h = th; c.tile_w = tw; c.dtype = dtype; c.rule = TRA_MASK_VOTE; c.budget_map = TRA_BUDGET_UNIFORM;
+  c.distance = dist; c.text_tokens = text; c.tau = 0.9f; c.gamma = 0.6f;
+  return c;
+}
+
+}  // namespace
+
+int main() {
+  const std::vector<tra_config> good = {
+      make(4, 8, 8, 64, 64, 8, 8, 0, TRA_FP32, TRA_DIST_2D),          // tiny
+      make(21, 30, 52, 128, 128, 8, 16, 0, TRA_BF16, TRA_DIST_2D),    // 480p
+      make(21, 45, 80, 128, 128, 8, 16, 0, TRA_BF16, TRA_DIST_2D),    // 720p
+      make(33, 45, 80, 128, 128, 8, 16, 256, TRA_BF16, TRA_DIST_2D),  // joint, 129 frames
+      make(3, 11, 29, 64, 128, 8, 16, 0, TRA_BF16, TRA_DIST_1D),      // ragged, 1-D
+      make(2, 9, 11, 128, 64, 8, 8, 50, TRA_FP32, TRA_DIST_2D),       // block 64, text
+      make(1, 1, 1, 128, 128, 8, 16, 0, TRA_BF16, TRA_DIST_2D),       // a single token
+      make(3, 7, 19, 128, 128, 5, 7, 77, TRA_FP32, TRA_DIST_1D),      // odd tiles, text, 1-D
+  };
+  for (size_t ci = 0; ci < good.size(); ++ci) {
+    const tra_config& c = good[ci];
+    const int ic = (int)ci;
+    std::string why;
+    expect(tra::validate_config(&c, &why) == TRA_OK, "valid config rejected", ic);
+    tra::HostTables t;
+    tra::build_host_tables(c, &t, true, true, true, true, c.dtype == TRA_BF16);
+    const int N = c.frames * c.height * c.width, S = N + c.text_tokens;
+    expect(t.N == N && t.S == S && t.NB == (S + c.block - 1) / c.block, "sizes", ic);
+    // the permutation is a bijection of [0, S), text tokens last and in order
+    std::vector<int> seen(S, 0);
+    bool in_range = (int)t.perm.size() == S;
+    for (int p = 0; in_range && p < S; ++p) {
+      in_range = t.perm[p] >= 0 && t.perm[p] < S;
+      if (in_range) ++seen[t.perm[p]];
+    }
+    expect(in_range, "perm out of range", ic);
+    bool bij = in_range;
+    for (int i = 0; bij && i < S; ++i) bij = seen[i] == 1;
+    expect(bij, "perm not a bijection", ic);
+    for (int p = N; p < S; ++p) expect(t.perm[p] == p, "text tokens reordered", ic);
+    // packed coordinates agree with the permutation
+    for (int p = 0; p < N; ++p) {
+      const int i = t.perm[p];
+      const int f = i / (c.height * c.width), x = (i / c.width) % c.height, y = i % c.width;
+      if (t.coord[p] != tra::pack_coord(f, x, y)) {
+        expect(false, "coord", ic);
+        break;
+      }
+    }
+    // thresholds: delta = 0 is n itself, non-increasing in delta
+    const int F = c.frames;
+    for (int n = 0; n <= t.n_cap; ++n) {
+      expect(t.thr[(size_t)n * F] == n, "thr[n][0] != n", ic);
+      for (int d = 1; d < F; ++d)
+        if (t.thr[(size_t)n * F + d] > t.thr[(size_t)n * F + d - 1]) { expect(false, "thr increasing", ic); break; }
+      for (int d = 1; d < F; ++d)
+        if (t.thr1[(size_t)n * F + d] > t.thr1[(size_t)n * F + d - 1]) { expect(false, "thr1 increasing", ic); break; }
+    }
+    // block boxes hold every video token of their block; counts add up
+    int video = 0, text = 0;
+    for (int u = 0; u < t.NB; ++u) {
+      const int32_t* bi = &t.blocks[(size_t)u * tra::kBlockInfo];
+      video += bi[6];
+      text += bi[9];
+      for (int p = u * c.block; p < std::min(S, (u + 1) * c.block) && p < N; ++p) {
+        const int i = t.perm[p];
+        const int f = i / (c.height * c.width), x = (i / c.width) % c.height, y = i % c.width;
+        if (f < bi[0] || f > bi[1] || x < bi[2] || x > bi[3] || y < bi[4] || y > bi[5] || i < bi[7] || i > bi[8]) {
+          expect(false, "token outside its block box", ic);
+          break;
+        }
+      }
+    }
+    expect(video == N && text == c.text_tokens, "block token counts", ic);
+    if (c.dtype == TRA_BF16) {
+      expect(t.kinfo.size() == (size_t)(t.NB + 1) * tra::kKeyInfo, "key-word table size", ic);
+      for (int p = 0; p < S; ++p) {
+        const uint32_t w = (uint32_t)t.kinfo[(size_t)(p / c.block) * tra::kKeyInfo + p % c.block];
+        if (p >= N) {
+          if (w != 1u << 31) { expect(false, "text key word", ic); break; }
+          continue;
+        }
+        const int i = t.perm[p];
+        const uint32_t base = c.distance == TRA_DIST_1D ? (uint32_t)i
+                                                        : (uint32_t)((i / c.width) % c.height) | ((uint32_t)(i % c.width) << 16);
+        const uint32_t flag = c.distance == TRA_DIST_1D ? 1u << 30 : 1u << 15;
+        if ((w & ~flag) != base) { expect(false, "key word", ic); break; }
+      }
+    }
+  }
+  // invalid configurations are rejected before any table is built
+  std::vector<tra_config> bad;
+  tra_config b0 = good[1]; b0.head_dim = 96; bad.push_back(b0);
+  tra_config b1 = good[1]; b1.frames = 0; bad.push_back(b1);
+  tra_config b2 = good[1]; b2.frames = 65; bad.push_back(b2);
+  tra_config b3 = good[1]; b3.width = 1024; bad.push_back(b3);
+  tra_config b4 = good[1]; b4.block = 64; bad.push_back(b4);  // bf16 needs 128
+  tra_config b5 = good[1]; b5.tau = 1.0f; bad.push_back(b5);
+  tra_config b6 = good[1]; b6.text_tokens = -1; bad.push_back(b6);
+  tra_config b7 = good[1]; b7.distance = 7; bad.push_back(b7);
+  for (size_t i = 0; i < bad.size(); ++i) {
+    std::string why;
+    expect(tra::validate_config(&bad[i], &why) != TRA_OK && !why.empty(), "invalid config accepted",
+           100 + (int)i);
+  }
+  std::string why;
+  expect(tra::validate_config(nullptr, &why) == TRA_ERR_INVALID_ARG, "NULL config", 200);
+  std::printf(failures ? "host tables: %d failure(s)\n" : "host tables: ok\n", failures);
+  return failures ? 1 : 0;
+}
