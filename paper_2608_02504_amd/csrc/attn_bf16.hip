@@ -1,9 +1,13 @@
 // bf16 attention family on gfx950 matrix cores: dense attention (Eq. 1),
 // block-sparse TRA attention (Eq. 16 at block granularity), its token-level
 // form (the token mask of Eq. 15 inside the retained blocks) and the
-// online-softmax entropy pass (App. C.2, Alg. 2), all from one 4-wave
-// template; plus an 8-wave split-key kernel for the entropy pass fused with
-// the dense output (at the end of the file).
+// online-softmax entropy pass (App. C.2, Alg. 2).  Three kernels:
+//   attn_k64_kernel   dense and block-sparse output, 64-key tiles, three
+//                     4-wave workgroups per CU;
+//   attn_bf16_kernel  token-level output and the entropy pass, 128-key tiles,
+//                     two 4-wave workgroups per CU;
+//   attn_fused_kernel the entropy pass fused with the dense output, 8 waves
+//                     splitting the keys of one query block.
 //
 // Layout pre-pass
 //   K and V are first gathered into tile-major order (Sec. 3.3: tokens of a
@@ -17,9 +21,10 @@
 // Work decomposition
 //   One workgroup (4 waves, 256 threads) per query-block row r = (b, h, u):
 //   128 queries, wave w owning queries [32w, 32w + 32).  It walks the key
-//   blocks of its row (all NB for dense; cols[r][0..cnt[r]) for sparse), 128
-//   keys per tile.  Two workgroups share a CU (64 KB of LDS each), so a SIMD
-//   can run one workgroup's matrix phase while the other is in its softmax.
+//   blocks of its row (all NB for dense; cols[r][0..cnt[r]) for sparse).
+//   Several workgroups share a CU, so a SIMD can run one workgroup's matrix
+//   phase while another is in its softmax: three with 64-key tiles (32 KB of
+//   LDS each), two with 128-key tiles (64 KB each).
 //
 // Per tile (split barriers)
 //   K and V^T go from HBM straight into LDS (global_load_lds_dwordx4 from a
@@ -30,7 +35,7 @@
 //
 // Matrix work (v_mfma_f32_32x32x16_bf16, fp32 accumulation)
 //   S^T = K Q^T: keys are the M side and the wave's 32 queries the N side, so a
-//   lane holds 64 scores of ONE query (row max / row sum are in-lane plus one
+//   lane holds the scores of ONE query (row max / row sum are in-lane plus one
 //   cross-half lane swap).  The bf16 probabilities stay in registers as the B
 //   operand of O^T += V^T P^T; K rows are loaded in an order that leaves every
 //   lane half holding 8 consecutive keys, the k-slice a V^T row chunk covers.
@@ -854,6 +859,229 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   }
 }
 
+// ------------------------------------------------------------ 64-key tiles
+// Dense / block-sparse attention with each 128-key block taken as two 64-key
+// tiles: per wave 32 scores and 16 probability pairs in flight instead of 64
+// and 32, and 32 KB of LDS per workgroup, so three workgroups (three waves per
+// SIMD) share a CU.  The V^T half-tile rows are 128 bytes, strided by the
+// block's 256-byte rows in HBM; their 16-byte chunks are XOR-swizzled so that
+// the PV operand reads hit every bank once.
+constexpr int kKT = 64;  // keys per tile
+
+// Lane offset within a 4 KB step of a V^T half-tile: row wave * 8 + lane / 8
+// of the step (32 rows of 64 keys), physical chunk lane % 8, which holds logical
+// chunk (lane % 8) ^ swz<8>(row); rows are 256 bytes apart in HBM.
+__device__ __forceinline__ uint32_t vt64_lane_off(int wave, int lane) {
+  const int row = wave * 8 + lane / 8;
+  return row * 256 + (((lane % 8) ^ swz<8>(row)) << 4);
+}
+
+template <int N, int SRC_STEP>
+__device__ __forceinline__ void issue_steps_strided(uint32_t lds_wave, const uint8_t* tile, uint32_t lane_off) {
+  if constexpr (N > 0) {
+    issue_steps_strided<N - 1, SRC_STEP>(lds_wave, tile, lane_off);
+    dma16<(N - 1) * 4096>(tile + (N - 1) * SRC_STEP, lane_off, lds_wave);
+  }
+}
+
+template <int D, bool SPARSE>
+__global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
+    uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N,
+    int n_pad, int NB, int rows, float scale_log2) {
+  using G = Geo<D>;
+  constexpr int KT_BYTES = kKT * D * 2;            // one 64-key tile of K or V^T
+  constexpr int STEPS = KT_BYTES / 4096;           // 4 KB copy steps per tile
+  __shared__ __attribute__((aligned(1024))) uint8_t smemK[KT_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t smemV[KT_BYTES];
+  extern __shared__ int32_t smemCols[];
+
+  int r = blockIdx.x;
+  if (SPARSE && order) {
+    r = order[blockIdx.x];
+    if (r < 0 || r >= rows) return;
+  } else {
+    r = xcd_row(blockIdx.x, rows);
+  }
+  const int bh = r / NB, u = r - bh * NB;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int col = lane & 31, half = lane >> 5;
+  const size_t head_off = (size_t)bh * N * D;
+  constexpr size_t kBlockBytes = (size_t)kBK * D * 2;
+  const uint8_t* Kb = (const uint8_t*)(ktile + (size_t)bh * n_pad * D);
+  const uint8_t* Vb = (const uint8_t*)(vtile + (size_t)bh * n_pad * D);
+  const uint32_t k_lds = (uint32_t)(uintptr_t)smemK + wave * 1024;
+  const uint32_t v_lds = (uint32_t)(uintptr_t)smemV + wave * 1024;
+  const uint32_t k_off = k_lane_off<D>(wave, lane);
+  const uint32_t v_off = vt64_lane_off(wave, lane);
+
+  const int qpos = u * kBQ + wave * 32 + col;
+  const bool qvalid = qpos < N;
+  const int qrow = qvalid ? perm[qpos] : 0;
+  bf16x8 qf[G::QK_STEPS];
+  {
+    const uint4* src = (const uint4*)(q + head_off + (size_t)qrow * D);
+#pragma unroll
+    for (int kk = 0; kk < G::QK_STEPS; ++kk) {
+      uint4 x = qvalid ? src[2 * kk + half] : make_uint4(0, 0, 0, 0);
+      qf[kk] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+  const int count = SPARSE ? min(max(cnt[r], 0), NB) : NB;
+  if constexpr (SPARSE) {
+    const int32_t* colp = cols + (size_t)r * NB;
+    for (int j = t; j < count; j += kThreads) smemCols[j] = colp[j];
+  }
+  wait_vm<0>();
+  lds_barrier();
+  const int krow = (col & ~15) | ((col & 15) ^ (((col >> 2) & 3) == 1 || ((col >> 2) & 3) == 2 ? 12 : 0));
+  const uint32_t kbase = krow * D * 2 + ((half ^ swz<G::CH>(krow)) << 4);
+  // V^T operand: row d = 32 dt + (lane % 32) of the half-tile (128-byte rows), chunk 2 ks + h
+  const uint32_t vbase = col * kKT * 2 + ((half ^ swz<8>(col)) << 4);
+
+  // Tile i of the row: block list[i / 2], keys [64 (i % 2), +64) of it; a
+  // list entry outside [0, NB) and a half past the last token are skipped.
+  // Returns the tile's packed (block, half) as 2 block + half, or -1 past the end.
+  auto next_valid = [&](int i, int* pos) -> int {
+    for (; i < 2 * count; ++i) {
+      const int c = SPARSE ? smemCols[i >> 1] : (i >> 1);
+      if (c >= 0 && c < NB && c * kBK + (i & 1) * kKT < N) {
+        *pos = i;
+        return __builtin_amdgcn_readfirstlane(2 * c + (i & 1));
+      }
+    }
+    *pos = 2 * count;
+    return -1;
+  };
+  auto k_src = [&](int bt) { return Kb + (bt >> 1) * kBlockBytes + (bt & 1) * KT_BYTES; };
+  auto v_src = [&](int bt) { return Vb + (bt >> 1) * kBlockBytes + (bt & 1) * (kKT * 2); };
+  auto issue_k = [&](int bt) { issue_steps<STEPS>(k_lds, k_src(bt), k_off); };
+  auto issue_v = [&](int bt) { issue_steps_strided<STEPS, 32 * 256>(v_lds, v_src(bt), v_off); };
+
+  f32x16 oacc[G::D_TILES];
+#pragma unroll
+  for (int i = 0; i < G::D_TILES; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
+  RowState st{-INFINITY, 0.f, 0.f};
+
+  int pos;
+  int bt_cur = next_valid(0, &pos);
+  int bt_nxt = bt_cur >= 0 ? next_valid(pos + 1, &pos) : -1;
+  if (bt_cur >= 0) {
+    issue_k(bt_cur);
+    issue_v(bt_cur);
+    for (;;) {
+      const bool has_next = bt_nxt >= 0;
+      wait_vm<STEPS>();  // K tile landed (V^T may still be in flight)
+      lds_barrier();
+      f32x16 s[2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
+      {
+        const uint32_t kb = opaque(kbase);
+        const lds_u8* kbuf = (const lds_u8*)smemK;
+#pragma unroll
+        for (int kk = 0; kk < G::QK_STEPS; ++kk) {
+          const uint32_t off = chunk_off(kb, kk);
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt) qk_step<D>(s[kt], kbuf, off, qf, kt, kk);
+        }
+        sched_reads_ahead<2 * G::QK_STEPS, 1, 4>();
+      }
+      lds_barrier();  // every wave is done with the K tile
+      if (has_next) issue_k(bt_nxt);
+      const int nv = N - (bt_cur >> 1) * kBK - (bt_cur & 1) * kKT;  // valid keys in this tile (> 0)
+      if (nv < kKT) {
+        const int base = 8 * half - nv;
+        const uint32_t neg = __float_as_uint(-1.0e30f);
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const uint32_t keep = (uint32_t)((kt * 32 + 16 * (e >> 3) + (e & 7) + base) >> 31);
+            s[kt][e] = __uint_as_float(((__float_as_uint(s[kt][e]) & keep) | (neg & ~keep)));
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
+      mx = max_halves(mx);
+      const float m_new = next_reference(st.m, mx * scale_log2);
+      const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
+      st.l *= sc;
+      st.m = m_new;
+      uint32_t pb[16];
+      float lsum = 0.f, asum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) tile_exp<true, false>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
+      st.l += lsum;
+      if (has_next) wait_vm<STEPS>();  // V^T landed (the next K tile may still be in flight)
+      else wait_vm<0>();
+      lds_barrier();
+      if (__ballot(sc != 1.0f) != 0) {
+#pragma unroll
+        for (int dt = 0; dt < G::D_TILES; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[dt][e] *= sc;
+      }
+      {
+        const uint32_t vb0 = opaque(vbase);
+        const lds_u8* vbuf = (const lds_u8*)smemV;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const uint32_t off = chunk_off(vb0, ks);
+          const int kt = ks >> 1, eb = (ks & 1) * 4;
+          const uint4 bw = make_uint4(pb[kt * 8 + eb], pb[kt * 8 + eb + 1], pb[kt * 8 + eb + 2], pb[kt * 8 + eb + 3]);
+#pragma unroll
+          for (int dt = 0; dt < G::D_TILES; ++dt) {
+            const bf16x8 va = lds_read16(vbuf, off + dt * 32 * kKT * 2);
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, __builtin_bit_cast(bf16x8, bw), oacc[dt], 0, 0, 0);
+          }
+        }
+        sched_reads_ahead<4 * G::D_TILES, 1, 4>();
+      }
+      lds_barrier();  // every wave is done with the V^T tile
+      if (has_next) issue_v(bt_nxt);
+      if (!has_next) break;
+      bt_cur = bt_nxt;
+      bt_nxt = next_valid(pos + 1, &pos);
+    }
+  }
+
+  const float l_tot = sum_halves(st.l);
+  if (!qvalid) return;
+  const size_t tok = (size_t)bh * N + qrow;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  uint16_t* dst = o + tok * D;
+#pragma unroll
+  for (int dt = 0; dt < G::D_TILES; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int d0 = dt * 32 + 8 * g + 4 * half;
+      uint2 w;
+      w.x = pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv);
+      w.y = pack_bf16x2(oacc[dt][4 * g + 2] * inv, oacc[dt][4 * g + 3] * inv);
+      *(uint2*)(dst + d0) = w;
+    }
+  if (half == 0 && lse) lse[tok] = l_tot > 0.f ? 0.69314718055994531f * (st.m + __log2f(l_tot)) : -INFINITY;
+}
+
+template <int D, bool SPARSE>
+void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  const size_t lds_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
+  hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE>), dim3(p.rows), dim3(kThreads), lds_bytes, s,
+                     (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cnt, a.cols, a.order,
+                     p.S, p.n_pad, p.NB, p.rows, scale_log2);
+}
+
 // ------------------------------------------------------------ fused entropy + dense output
 // The warm-up step's call (App. C.2, Alg. 2 with O): entropy and the dense
 // output in one pass.  Its per-wave state (scores, P, O, Q and the entropy
@@ -1089,10 +1317,10 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
   }
   if (a.sparse && a.radius_sq && p.cfg.distance == TRA_DIST_1D) launch_variant<D, true, true, false, 2>(p, a, s);
   else if (a.sparse && a.radius_sq) launch_variant<D, true, true, false, 1>(p, a, s);
-  else if (a.sparse) launch_variant<D, true, true, false>(p, a, s);
+  else if (a.sparse) launch_k64<D, true>(p, a, s);
   else if (a.entropy && a.o) launch_fused_entropy_output<D>(p, a, s);
   else if (a.entropy) launch_variant<D, false, false, true>(p, a, s);
-  else launch_variant<D, false, true, false>(p, a, s);
+  else launch_k64<D, false>(p, a, s);
   return hipGetLastError();
 }
 

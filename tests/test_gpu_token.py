@@ -104,15 +104,24 @@ def test_token_attention_forced_radii_1d_and_2d(name, radius):
 
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny", "joint_bf16_d128"])
-def test_token_full_radius_equals_sparse_bitwise(name):
+def test_token_full_radius_matches_sparse(name):
     """Every radius FULL: every query covers every key of its retained blocks,
-    so token-level attention is the block-sparse call, bit for bit."""
+    so token-level attention computes the block-sparse call.  The bf16 kernels
+    walk the keys in tiles of different sizes (the softmax reference moves at
+    different points), so the two agree to rounding, not bit for bit; fp32
+    shares one kernel and stays bitwise."""
     _gpu()
     import torch
-    run = Run(W[name], radius_override=2 ** 31 - 1)
+    w = W[name]
+    run = Run(w, radius_override=2 ** 31 - 1)
     o, lse = _token_call(run)
-    assert torch.equal(o, run.O_sp)
-    assert torch.equal(lse, run.lse_sp)
+    if w.dtype == "fp32":
+        assert torch.equal(o, run.O_sp) and torch.equal(lse, run.lse_sp)
+        return
+    err = (o.float() - run.O_sp.float()).abs().max().item()
+    assert err <= TOL_O_BF16, f"token vs sparse max-abs {err:.3e}"
+    lerr = (lse - run.lse_sp).abs().max().item()
+    assert lerr <= 1e-4 + 1e-5 * run.lse_sp.abs().max().item(), f"token vs sparse lse {lerr:.3e}"
 
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "tiny"])
