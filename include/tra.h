@@ -57,9 +57,11 @@
  * 2 x batch x heads x NB x 128 x head_dim x 2 bytes into which every
  * attention call (tra_entropy, tra_sparse_attention, tra_token_attention,
  * tra_dense_attention)
- * first rewrites K and V in tile-major order (V transposed per block).  Calls
+ * first rewrites K and V in tile-major order (V transposed per block), and
+ * 512 bytes of row-queue counters that the block-sparse and dense calls reset
+ * and then draw their query-block rows from.  Calls
  * that share a plan must therefore not overlap in time on different streams
- * when they use a workspace (those three calls on bf16 plans, and
+ * when they use a workspace (those calls on bf16 plans, and
  * tra_build_block_mask with a non-NULL order); calls on one stream are ordered
  * and safe.  Otherwise the plan is immutable after creation.  No C++
  * exception crosses this ABI.  On failure, tra_last_error() returns a message

@@ -111,6 +111,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_kt);
   (void)hipFree(p->d_vt);
   (void)hipFree(p->d_kinfo);
+  (void)hipFree(p->d_row_ctr);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -140,6 +141,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
     tra_plan p = new tra_plan_s();
     p->cfg = *cfg;
     p->device = dev;
+    p->n_cu = prop.multiProcessorCount;
     p->N = t.N;
     p->S = t.S;
     p->NB = t.NB;
@@ -171,7 +173,8 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       const size_t bytes = (size_t)cfg->batch * cfg->heads * p->n_pad * cfg->head_dim * sizeof(uint16_t);
       if ((e = hipMalloc((void**)&p->d_kt, bytes)) != hipSuccess ||
           (e = hipMalloc((void**)&p->d_vt, bytes)) != hipSuccess ||
-          (e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess) {
+          (e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_row_ctr, tra::kRowCounters * sizeof(int32_t))) != hipSuccess) {
         tra_plan_destroy(p);
         return fail(TRA_ERR_ALLOC, std::string("plan K/V workspace: ") + hipGetErrorString(e));
       }

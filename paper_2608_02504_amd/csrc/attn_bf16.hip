@@ -45,6 +45,7 @@
 //   On a max increase m -> m': l <- 2^{m-m'} l, a <- 2^{m-m'} (a + l (m - m')).
 //   H = ln(l) - ln(2) a / l  (nats)  == log Z - sum_j p_j s_j (App. C.2).
 //   Each lane keeps l and a over its own keys; the halves are added at the end.
+#include <algorithm>
 #include <climits>
 #include <cmath>
 
@@ -885,27 +886,17 @@ __device__ __forceinline__ void issue_steps_strided(uint32_t lds_wave, const uin
 }
 
 template <int D, bool SPARSE>
-__global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
+__device__ __forceinline__ void k64_row(
+    int r, uint8_t* smemK, uint8_t* smemV, int32_t* smemCols,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
     uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N,
-    int n_pad, int NB, int rows, float scale_log2) {
+    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, int N,
+    int n_pad, int NB, float scale_log2) {
   using G = Geo<D>;
   constexpr int KT_BYTES = kKT * D * 2;            // one 64-key tile of K or V^T
   constexpr int STEPS = KT_BYTES / 4096;           // 4 KB copy steps per tile
-  __shared__ __attribute__((aligned(1024))) uint8_t smemK[KT_BYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t smemV[KT_BYTES];
-  extern __shared__ int32_t smemCols[];
-
-  int r = blockIdx.x;
-  if (SPARSE && order) {
-    r = order[blockIdx.x];
-    if (r < 0 || r >= rows) return;
-  } else {
-    r = xcd_row(blockIdx.x, rows);
-  }
   const int bh = r / NB, u = r - bh * NB;
-  const int t = threadIdx.x, lane = t & 63;
+  const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int col = lane & 31, half = lane >> 5;
   const size_t head_off = (size_t)bh * N * D;
@@ -1073,13 +1064,88 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
   if (half == 0 && lse) lse[tok] = l_tot > 0.f ? 0.69314718055994531f * (st.m + __log2f(l_tot)) : -INFINITY;
 }
 
+// Row queue of the persistent kernel (thread 0 of a workgroup only).  Without a
+// caller order the rows are split into 8 contiguous ranges, one per XCD (the
+// workgroup with index b runs on XCD b mod 8), each drained through its own
+// counter: the rows an XCD has in flight are neighbouring query blocks of one
+// head, which share most key tiles in its L2.  A workgroup whose range is
+// drained takes rows from the next ranges in turn, so an XCD that runs at a
+// higher clock ends up doing more rows.  With a caller order, one counter walks
+// it (entries outside [0, rows) are skipped).  Returns -1 once all is drained.
+// ctr: kRowCounters ints, zero before the launch; counter x at ctr[16 x].
+__device__ __forceinline__ int k64_next_row(int32_t* ctr, const int32_t* __restrict__ order, int rows, int xcd,
+                                            int& steal) {
+  if (order) {
+    for (;;) {
+      const int k = atomicAdd(&ctr[0], 1);
+      if (k >= rows) return -1;
+      const int r = order[k];
+      if (r >= 0 && r < rows) return r;
+    }
+  }
+  const int per = rows / 8, rem = rows % 8;
+  while (steal < 8) {
+    const int qd = (xcd + steal) & 7;
+    const int beg = qd * per + min(qd, rem), n = per + (qd < rem ? 1 : 0);
+    const int k = atomicAdd(&ctr[qd * 16], 1);
+    if (k < n) return beg + k;
+    ++steal;
+  }
+  return -1;
+}
+
+// Persistent kernel: as many workgroups as fit on the GPU (three per CU), each
+// taking rows from the row queue until it is drained.  Every row starts with a
+// workgroup barrier (after its block list is staged), which also orders the
+// next s_row write after every wave's read of the current one.
+template <int D, bool SPARSE>
+__global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
+    uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N,
+    int n_pad, int NB, int rows, float scale_log2, int32_t* __restrict__ ctr) {
+  constexpr int KT_BYTES = kKT * D * 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t smemK[KT_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t smemV[KT_BYTES];
+  extern __shared__ int32_t smemCols[];
+  __shared__ int s_row, s_steal;  // thread 0's queue state lives in LDS, not in a register
+  if (threadIdx.x == 0) s_steal = 0;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int steal = s_steal;
+      s_row = k64_next_row(ctr, SPARSE ? order : nullptr, rows, blockIdx.x & 7, steal);
+      s_steal = steal;
+    }
+    __syncthreads();
+    const int r = s_row;
+    if (r < 0) break;
+    k64_row<D, SPARSE>(r, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cnt, cols, N, n_pad, NB,
+                       scale_log2);
+  }
+}
+
+// Zeroes the row-queue counters (a kernel rather than a memset, so that the
+// launch sequence also replays correctly inside a captured graph).
+__global__ void k64_reset_counters(int32_t* ctr) {
+  if (threadIdx.x < kRowCounters) ctr[threadIdx.x] = 0;
+}
+
 template <int D, bool SPARSE>
 void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const size_t lds_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
-  hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE>), dim3(p.rows), dim3(kThreads), lds_bytes, s,
-                     (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cnt, a.cols, a.order,
-                     p.S, p.n_pad, p.NB, p.rows, scale_log2);
+  // as many workgroups as can be resident at once (the occupancy the kernel's
+  // registers and LDS allow), capped by the row count
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_k64_kernel<D, SPARSE>, kThreads, lds_bytes) !=
+          hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  const int grid = std::min(p.rows, per_cu * std::max(p.n_cu, 1));
+  hipLaunchKernelGGL(k64_reset_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE>), dim3(grid), dim3(kThreads), lds_bytes, s, (const uint16_t*)a.q,
+                     p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB,
+                     p.rows, scale_log2, p.d_row_ctr);
 }
 
 // ------------------------------------------------------------ fused entropy + dense output

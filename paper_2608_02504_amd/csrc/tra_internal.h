@@ -26,6 +26,7 @@ constexpr int kKeyInfo = 128;  // ints per key block in the key-info table
 constexpr int kMaxFrames = 64;
 constexpr int kMaxBlocks = 4096;
 constexpr int kSortChunk = 256;
+constexpr int kRowCounters = 128;  // ints of the attention row-queue counters
 
 // Host-side tables of one shape (plan.cpp).
 struct HostTables {
@@ -73,6 +74,10 @@ struct tra_plan_s {
   // the key side of the token mask inside a tile.
   int32_t* d_kinfo = nullptr;
   int32_t thr_max = 0;  // largest entry of the plan's threshold table
+  // bf16 plans: row-queue counters of the persistent attention kernel
+  // (kRowCounters ints, reset by each call on its stream), and the CU count
+  int32_t* d_row_ctr = nullptr;
+  int32_t n_cu = 0;
 };
 
 namespace tra {

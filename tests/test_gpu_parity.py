@@ -270,6 +270,52 @@ def test_out_of_range_column_ids_are_skipped(name):
     assert torch.equal(got_l, ref_l)
 
 
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny"])
+def test_row_schedule_does_not_change_results(name):
+    """Rows are independent: the schedule (per-XCD row queues without an
+    order, the heaviest-first order, a random permutation, an order with
+    out-of-range entries that are skipped) changes only which workgroup
+    computes a row, and each result is bitwise the same; repeated calls start
+    from freshly reset row queues."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    run = Run(SMALL[name])
+    rows = run.plan.rows
+    dev = run.q.device
+    rng = np.random.default_rng(11)
+    perm = rng.permutation(rows).astype(np.int32)
+    padded = np.insert(perm, rng.integers(0, rows, 5), [-1, rows, -3, rows + 7, -1]).astype(np.int32)[:rows]
+    kept = set(int(r) for r in padded if 0 <= r < rows)
+    orders = [None, run.order, torch.from_numpy(perm).to(dev), None]
+    outs = []
+    for od in orders:
+        o, l = torch.empty_like(run.O_sp), torch.empty_like(run.lse_sp)
+        tra.tra_sparse_attention(run.plan, run.q, run.k, run.v, run.cnt, run.cols, od, o, l)
+        torch.cuda.synchronize()
+        outs.append((o, l))
+    for o, l in outs:
+        assert torch.equal(o, outs[0][0]) and torch.equal(l, outs[0][1])
+    # rows missing from the order (entries out of range) are not computed
+    o = torch.full_like(run.O_sp, 7.0)
+    tra.tra_sparse_attention(run.plan, run.q, run.k, run.v, run.cnt, run.cols,
+                             torch.from_numpy(padded).to(dev), o, None)
+    torch.cuda.synchronize()
+    NB = run.plan.n_blocks
+    perm_tok = OracleTables(run.w).perm
+    S = o.shape[2]
+    blk = np.arange(S) // run.w.block                    # tile-major position -> block
+    for r in range(rows):
+        bh, u = divmod(r, NB)
+        b, h = divmod(bh, o.shape[1])
+        toks = perm_tok[(blk == u)]
+        got = o[b, h, toks]
+        if r in kept:
+            assert torch.equal(got, outs[0][0][b, h, toks]), r
+        else:
+            assert bool((got == 7.0).all()), r
+
+
 def test_determinism_bitwise():
     _gpu()
     import torch
