@@ -451,6 +451,43 @@ __device__ __forceinline__ int xcd_row(int b, int rows) {
   return x * per + min(x, rem) + k;
 }
 
+// Row queue of the persistent attention kernels (thread 0 of a workgroup only).  Without a
+// caller order the rows are split into 8 contiguous ranges, one per XCD (the
+// workgroup with index b runs on XCD b mod 8), each drained through its own
+// counter: the rows an XCD has in flight are neighbouring query blocks of one
+// head, which share most key tiles in its L2.  A workgroup whose range is
+// drained takes rows from the next ranges in turn, so an XCD that runs at a
+// higher clock ends up doing more rows.  With a caller order, one counter walks
+// it (entries outside [0, rows) are skipped).  Returns -1 once all is drained.
+// ctr: kRowCounters ints, zero before the launch; counter x at ctr[16 x].
+__device__ __forceinline__ int next_row(int32_t* ctr, const int32_t* __restrict__ order, int rows, int xcd,
+                                            int& steal) {
+  if (order) {
+    for (;;) {
+      const int k = atomicAdd(&ctr[0], 1);
+      if (k >= rows) return -1;
+      const int r = order[k];
+      if (r >= 0 && r < rows) return r;
+    }
+  }
+  const int per = rows / 8, rem = rows % 8;
+  while (steal < 8) {
+    const int qd = (xcd + steal) & 7;
+    const int beg = qd * per + min(qd, rem), n = per + (qd < rem ? 1 : 0);
+    const int k = atomicAdd(&ctr[qd * 16], 1);
+    if (k < n) return beg + k;
+    ++steal;
+  }
+  return -1;
+}
+
+// Zeroes the row-queue counters (a kernel rather than a memset, so that the
+// launch sequence also replays correctly inside a captured graph).
+__global__ void reset_row_counters(int32_t* ctr) {
+  if (threadIdx.x < kRowCounters) ctr[threadIdx.x] = 0;
+}
+
+
 // ------------------------------------------------------------ softmax and copy helpers
 // Row max of a score tile as a max3 tree (short dependency chains), folded into
 // the running state like tile_max.
@@ -604,39 +641,24 @@ __device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, floa
   }
 }
 
-// TOK (sparse only): 0 block granular; 1 token mask with the 2-D distance,
-// 2 with the 1-D sequence distance (Eq. 15 inside the listed blocks).
-template <int D, bool SPARSE, bool PV, bool ENT, int OCC, int TOK = 0>
-__global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
+// One query-block row r of the 128-key-tile kernel.  LDS: smemK / smemV the K
+// and V^T tiles, smemKinfo (token variant) the key words of the current and
+// the next tile (a 1 KB copy each, of which the first 512 B are the tile's),
+// smemCols the row's key-block list (NB entries for the sparse variant), read
+// once so that the tile loop issues no global loads of its own (a wait for one
+// would also drain the tiles in flight); the token variant then keeps each
+// query's thresholds by frame distance after it, [128][F] uint16.
+template <int D, bool SPARSE, bool PV, bool ENT, int TOK>
+__device__ __forceinline__ void bf16_row(
+    int r, uint8_t* smemK, uint8_t* smemV, uint8_t* smemKinfo, int32_t* smemCols,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
     const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ lse,
     float* __restrict__ entropy, const int32_t* __restrict__ perm, const int32_t* __restrict__ cnt,
-    const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N, int n_pad, int NB,
-    int rows, float scale_log2, TokArgs tk) {
+    const int32_t* __restrict__ cols, int N, int n_pad, int NB, float scale_log2, const TokArgs& tk) {
   using G = Geo<D>;
-  constexpr int TILE = kBK * D * 2;
-  __shared__ __attribute__((aligned(1024))) uint8_t smemK[TILE];
-  __shared__ __attribute__((aligned(1024))) uint8_t smemV[PV ? TILE : 16];
-  // token variant: key words of the current and the next tile (a 1 KB copy
-  // each, of which the first 512 B are the tile's)
-  __shared__ __attribute__((aligned(16))) uint8_t smemKinfo[TOK ? 2 * 1024 : 16];
-  // the row's key-block list (dynamic LDS, NB entries for the sparse variant),
-  // read once so that the tile loop issues no global loads of its own (a wait
-  // for one would also drain the tiles in flight); the token variant then
-  // keeps each query's thresholds by frame distance, [128][F] uint16
-  extern __shared__ int32_t smemCols[];
   uint16_t* thrq = (uint16_t*)(smemCols + ((NB + 3) & ~3));
-
-  int r = blockIdx.x;
-  if (SPARSE && order) {
-    r = order[blockIdx.x];
-    if (r < 0 || r >= rows) return;
-  }
-  else {
-    r = xcd_row(blockIdx.x, rows);
-  }
   const int bh = r / NB, u = r - bh * NB;
-  const int t = threadIdx.x, lane = t & 63;
+  const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int col = lane & 31, half = lane >> 5;
   const size_t head_off = (size_t)bh * N * D;
@@ -860,6 +882,39 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   }
 }
 
+// TOK (sparse only): 0 block granular; 1 token mask with the 2-D distance,
+// 2 with the 1-D sequence distance (Eq. 15 inside the listed blocks).
+// Persistent: as many workgroups as can be resident, each taking rows from the
+// row queue until it is drained (the first barrier of every row, after its list
+// is staged, orders the next s_row write after every wave's read).
+template <int D, bool SPARSE, bool PV, bool ENT, int OCC, int TOK = 0>
+__global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
+    const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ lse,
+    float* __restrict__ entropy, const int32_t* __restrict__ perm, const int32_t* __restrict__ cnt,
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N, int n_pad, int NB,
+    int rows, float scale_log2, TokArgs tk, int32_t* __restrict__ ctr) {
+  constexpr int TILE = kBK * D * 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t smemK[TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t smemV[PV ? TILE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t smemKinfo[TOK ? 2 * 1024 : 16];
+  extern __shared__ int32_t smemCols[];
+  __shared__ int s_row, s_steal;  // thread 0's queue state lives in LDS, not in a register
+  if (threadIdx.x == 0) s_steal = 0;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int steal = s_steal;
+      s_row = next_row(ctr, SPARSE ? order : nullptr, rows, blockIdx.x & 7, steal);
+      s_steal = steal;
+    }
+    __syncthreads();
+    const int r = s_row;
+    if (r < 0) break;
+    bf16_row<D, SPARSE, PV, ENT, TOK>(r, smemK, smemV, smemKinfo, smemCols, q, ktile, vtile, o, lse, entropy,
+                                      perm, cnt, cols, N, n_pad, NB, scale_log2, tk);
+  }
+}
+
 // ------------------------------------------------------------ 64-key tiles
 // Dense / block-sparse attention with each 128-key block taken as two 64-key
 // tiles: per wave 32 scores and 16 probability pairs in flight instead of 64
@@ -1064,36 +1119,6 @@ __device__ __forceinline__ void k64_row(
   if (half == 0 && lse) lse[tok] = l_tot > 0.f ? 0.69314718055994531f * (st.m + __log2f(l_tot)) : -INFINITY;
 }
 
-// Row queue of the persistent kernel (thread 0 of a workgroup only).  Without a
-// caller order the rows are split into 8 contiguous ranges, one per XCD (the
-// workgroup with index b runs on XCD b mod 8), each drained through its own
-// counter: the rows an XCD has in flight are neighbouring query blocks of one
-// head, which share most key tiles in its L2.  A workgroup whose range is
-// drained takes rows from the next ranges in turn, so an XCD that runs at a
-// higher clock ends up doing more rows.  With a caller order, one counter walks
-// it (entries outside [0, rows) are skipped).  Returns -1 once all is drained.
-// ctr: kRowCounters ints, zero before the launch; counter x at ctr[16 x].
-__device__ __forceinline__ int k64_next_row(int32_t* ctr, const int32_t* __restrict__ order, int rows, int xcd,
-                                            int& steal) {
-  if (order) {
-    for (;;) {
-      const int k = atomicAdd(&ctr[0], 1);
-      if (k >= rows) return -1;
-      const int r = order[k];
-      if (r >= 0 && r < rows) return r;
-    }
-  }
-  const int per = rows / 8, rem = rows % 8;
-  while (steal < 8) {
-    const int qd = (xcd + steal) & 7;
-    const int beg = qd * per + min(qd, rem), n = per + (qd < rem ? 1 : 0);
-    const int k = atomicAdd(&ctr[qd * 16], 1);
-    if (k < n) return beg + k;
-    ++steal;
-  }
-  return -1;
-}
-
 // Persistent kernel: as many workgroups as fit on the GPU (three per CU), each
 // taking rows from the row queue until it is drained.  Every row starts with a
 // workgroup barrier (after its block list is staged), which also orders the
@@ -1113,7 +1138,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
   for (;;) {
     if (threadIdx.x == 0) {
       int steal = s_steal;
-      s_row = k64_next_row(ctr, SPARSE ? order : nullptr, rows, blockIdx.x & 7, steal);
+      s_row = next_row(ctr, SPARSE ? order : nullptr, rows, blockIdx.x & 7, steal);
       s_steal = steal;
     }
     __syncthreads();
@@ -1124,25 +1149,22 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
   }
 }
 
-// Zeroes the row-queue counters (a kernel rather than a memset, so that the
-// launch sequence also replays correctly inside a captured graph).
-__global__ void k64_reset_counters(int32_t* ctr) {
-  if (threadIdx.x < kRowCounters) ctr[threadIdx.x] = 0;
+// Grid of a persistent attention kernel: as many workgroups as can be resident
+// at once (the occupancy its registers and LDS allow), capped by the row count.
+template <typename K>
+int resident_grid(K kernel, size_t lds_bytes, const tra_plan_s& p) {
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_bytes) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  return std::min(p.rows, per_cu * std::max(p.n_cu, 1));
 }
 
 template <int D, bool SPARSE>
 void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const size_t lds_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
-  // as many workgroups as can be resident at once (the occupancy the kernel's
-  // registers and LDS allow), capped by the row count
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_k64_kernel<D, SPARSE>, kThreads, lds_bytes) !=
-          hipSuccess ||
-      per_cu < 1)
-    per_cu = 1;
-  const int grid = std::min(p.rows, per_cu * std::max(p.n_cu, 1));
-  hipLaunchKernelGGL(k64_reset_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  const int grid = resident_grid(attn_k64_kernel<D, SPARSE>, lds_bytes, p);
+  hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE>), dim3(grid), dim3(kThreads), lds_bytes, s, (const uint16_t*)a.q,
                      p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB,
                      p.rows, scale_log2, p.d_row_ctr);
@@ -1361,9 +1383,11 @@ void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   if (TOK != 0) lds_bytes += (size_t)kBQ * p.cfg.frames * sizeof(uint16_t);
   const TokArgs tk{a.radius_sq, p.cfg.distance == TRA_DIST_1D ? p.d_thr1 : p.d_thr, p.d_kinfo, p.d_blocks,
                    p.d_coord, p.N, p.cfg.frames, p.n_cap};
-  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>), dim3(p.rows), dim3(kThreads), lds_bytes, s,
+  const int grid = resident_grid(attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>, lds_bytes, p);
+  hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>), dim3(grid), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
-                     a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2, tk);
+                     a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2, tk, p.d_row_ctr);
 }
 
 template <int D>
