@@ -441,16 +441,6 @@ __device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restr
     }
 }
 
-// Row of the workgroup with index b when workgroups are dealt to the 8 XCDs
-// round-robin by index: each XCD gets a contiguous range of rows (same head,
-// neighbouring query blocks, largely the same key tiles), so its L2 serves
-// them together.  A bijection of [0, rows): XCD x holds rows / 8 + (x < rows % 8).
-__device__ __forceinline__ int xcd_row(int b, int rows) {
-  const int x = b & 7, k = b >> 3;
-  const int per = rows >> 3, rem = rows & 7;
-  return x * per + min(x, rem) + k;
-}
-
 // Row queue of the persistent attention kernels (thread 0 of a workgroup only).  Without a
 // caller order the rows are split into 8 contiguous ranges, one per XCD (the
 // workgroup with index b runs on XCD b mod 8), each drained through its own
@@ -1198,21 +1188,20 @@ void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
 // about one and a half phases to land.
 constexpr int kFusedThreads = 512;
 
+// One query-block row r of the fused kernel.  smem: per group a K tile, then a
+// V^T tile; smemState: group 1's (m, l, a) per query, for the merge.
 template <int D>
-__global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
-    const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ entropy,
-    const int32_t* __restrict__ perm, int N, int n_pad, int NB, int rows, float scale_log2) {
+__device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState,
+                                          const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
+                                          const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o,
+                                          float* __restrict__ entropy, const int32_t* __restrict__ perm, int N,
+                                          int n_pad, int NB, float scale_log2) {
   using G = Geo<D>;
   constexpr int TILE = kBK * D * 2;
   constexpr int GROUP_BYTES = 2 * TILE;  // K tile, then V^T tile
   constexpr int KS = TileCopy<D>::STEPS;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * GROUP_BYTES];
-  __shared__ float smemState[3 * kBQ];  // group 1's (m, l, a) per query, for the merge
-
-  const int r = xcd_row(blockIdx.x, rows);
   const int bh = r / NB, u = r - bh * NB;
-  const int t = threadIdx.x, lane = t & 63;
+  const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int g = wave >> 2, w4 = wave & 3;
   const int col = lane & 31, half = lane >> 5;
@@ -1368,12 +1357,45 @@ __global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
   if (half == 0) entropy[tok] = 0.69314718055994531f * (__log2f(l_tot) - a_tot / l_tot);
 }
 
+// Persistent: one workgroup per CU, taking rows from the per-XCD row queues
+// until they are drained (the first barrier of every row orders the next
+// s_row write after every wave's read of the current one).
+template <int D>
+__global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
+    const uint16_t* __restrict__ vtile, uint16_t* __restrict__ o, float* __restrict__ entropy,
+    const int32_t* __restrict__ perm, int N, int n_pad, int NB, int rows, float scale_log2,
+    int32_t* __restrict__ ctr) {
+  constexpr int TILE = kBK * D * 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILE];
+  __shared__ float smemState[3 * kBQ];
+  __shared__ int s_row, s_steal;
+  if (threadIdx.x == 0) s_steal = 0;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int steal = s_steal;
+      s_row = next_row(ctr, nullptr, rows, blockIdx.x & 7, steal);
+      s_steal = steal;
+    }
+    __syncthreads();
+    const int r = s_row;
+    if (r < 0) break;
+    fused_row<D>(r, smem, smemState, q, ktile, vtile, o, entropy, perm, N, n_pad, NB, scale_log2);
+  }
+}
+
 template <int D>
 void launch_fused_entropy_output(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
-  hipLaunchKernelGGL((attn_fused_kernel<D>), dim3(p.rows), dim3(kFusedThreads), 0, s, (const uint16_t*)a.q,
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_fused_kernel<D>, kFusedThreads, 0) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  const int grid = std::min(p.rows, per_cu * std::max(p.n_cu, 1));
+  hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  hipLaunchKernelGGL((attn_fused_kernel<D>), dim3(grid), dim3(kFusedThreads), 0, s, (const uint16_t*)a.q,
                      p.d_kt, p.d_vt, (uint16_t*)a.o, a.entropy, p.d_perm, p.S, p.n_pad, p.NB, p.rows,
-                     scale_log2);
+                     scale_log2, p.d_row_ctr);
 }
 
 template <int D, bool SPARSE, bool PV, bool ENT, int TOK = 0>
