@@ -43,7 +43,7 @@ class Run:
     """All stage outputs of one pass of the path on the GPU."""
 
     def __init__(self, w, rule="vote", with_order=True, inputs=None, radius_override=None,
-                 budget="uniform", distance="2d"):
+                 budget="uniform", distance="2d", entropy_override=None):
         import torch
         self.w = w
         self.cfg = tra.Config.from_workload(w, rule=rule, budget=budget, distance=distance)
@@ -74,7 +74,13 @@ class Run:
 
         tra.tra_entropy(self.plan, q, k, v, self.O_ent, self.H)
         tra.tra_entropy(self.plan, q, k, None, None, self.H_only)
-        tra.tra_budget_radius(self.plan, self.H, self.budget, self.rad)
+        # entropy_override: one constant entropy for every token feeds the budget
+        # and radius stage (a uniform budget, as in the paper's ablation), so
+        # the mask keeps a chosen fraction of the blocks
+        self.H_budget = self.H
+        if entropy_override is not None:
+            self.H_budget = torch.full_like(self.H, float(entropy_override))
+        tra.tra_budget_radius(self.plan, self.H_budget, self.budget, self.rad)
         if radius_override is not None:
             self.rad[:, :, :w.n_video] = int(radius_override)
         tra.tra_build_block_mask(self.plan, self.rad, self.mask, self.cnt, self.cols, self.order)
@@ -167,7 +173,7 @@ def check_head(run: Run, tabs: OracleTables, b: int, h: int, blocks, tol_o: floa
     kh_gpu = run.budget[b, h].cpu().numpy()[rows]
     n_gpu = run.rad[b, h].cpu().numpy()[rows]
     assert (kh_gpu[~video] == N).all() and (n_gpu[~video] == O.RADIUS_FULL).all(), "text budget/radius"
-    Hv, rv = H_gpu[video], rows[video]
+    Hv, rv = run.H_budget[b, h].double().cpu().numpy()[rows][video], rows[video]
     if run.cfg.budget == "lognormal":
         khat_ref = O.token_budget_lognormal(Hv, w.tau, N)
         sigma = np.sqrt(2.0 * np.maximum(0.0, math.log(N) - Hv))

@@ -327,10 +327,10 @@ def test_determinism_bitwise():
         assert torch.equal(getattr(a, name), getattr(b, name)), name
 
 
-def _sampled(name, heads=None):
+def _sampled(name, heads=None, **run_kw):
     _gpu()
     w = synth.workload(name)
-    run = Run(w)
+    run = Run(w, **run_kw)
     tabs = OracleTables(w)
     report = {}
     samples = sample_blocks(w, BLOCKS_PER_HEAD, seed=2024)
@@ -358,3 +358,17 @@ def test_wan14b_720p_sampled():
 @pytest.mark.slow
 def test_hunyuan_720p_sampled():
     _sampled("hunyuan_720p")
+
+
+@pytest.mark.slow
+def test_wan14b_720p_sampled_at_paper_density():
+    """The headline shape with partial block lists, as the density sweep runs
+    it: one constant entropy ln(7997 / tau) for every token (a uniform budget
+    of 7,997 keys) keeps ~15 % of the blocks; sparse attention without a row
+    order (the per-XCD row queues) is checked on sampled query blocks of 8 of
+    the 40 heads, with every stage before it."""
+    w = synth.workload("wan14b_720p")
+    run = _sampled("wan14b_720p", heads=range(0, 40, 5), with_order=False,
+                   entropy_override=float(np.log(7997 / w.tau)))
+    rho = retained_fraction(run)
+    assert 0.12 < rho < 0.18, rho
