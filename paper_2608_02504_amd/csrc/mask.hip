@@ -53,6 +53,9 @@ __device__ __forceinline__ void position(int32_t c, int H, int W, int* a, int* b
   }
 }
 
+typedef short short2_t __attribute__((ext_vector_type(2)));
+typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
+
 template <int B, int RULE, int DIST>
 __global__ __launch_bounds__(256) void block_mask_kernel(
     const int32_t* __restrict__ radius_sq, const int32_t* __restrict__ perm,
@@ -60,9 +63,16 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
     const int32_t* __restrict__ binfo, uint8_t* __restrict__ mask, int32_t* __restrict__ cnt,
     int32_t* __restrict__ cols, int N, int S, int NB, int F, int H, int W, int n_cap) {
   constexpr int QPL = B / 64;  // queries (and keys) per lane
-  __shared__ int32_t s_T[B * kMaxFrames];  // s_T[q*F + delta]: distance threshold of query q
+  extern __shared__ int32_t s_T[];         // [B * F]: s_T[q*F + delta], distance threshold of query q
   __shared__ int32_t s_c[B];               // packed coordinate of query q
   __shared__ uint8_t s_keep[kMaxBlocks];
+  // per wave: the partial queries of the current key block, two per entry, as
+  // 16-bit halves of four words (x, y, threshold + 1 for each of the block's two
+  // frames); read back with one broadcast load per entry
+  __shared__ uint32_t s_pairs[4][B / 2][4];
+  // 16-bit packed distances are exact while every squared distance and
+  // threshold stays below 2^15 (the plan caps H and W, not their squares)
+  const bool packed16 = DIST == TRA_DIST_2D && n_cap < 32767;
 
   const int row = blockIdx.x;
   const int bh = row / NB, u = row - bh * NB;
@@ -165,7 +175,71 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
           position<DIST>(cc, H, W, &kx[s], &ky[s], &kf[s]);
           c[s] = n_all;
         }
-        if (fmax - fmin <= 1) {
+        if (packed16 && fmax - fmin <= 1) {
+          // Block v spans at most two frames, so a partial query needs two
+          // thresholds (keys of frame fmin, keys of frame fmax).  The wave's
+          // partial queries are listed in LDS in pairs (16-bit halves), and each
+          // step tests two queries against this lane's keys with packed 16-bit
+          // arithmetic: D = dx^2 + dy^2 per half, covered iff D - (T + 1) < 0,
+          // the sign bits summed into a packed count per key.
+          uint16_t* lst = (uint16_t*)&s_pairs[wave][0][0];
+          int P = 0;
+#pragma unroll
+          for (int s = 0; s < QPL; ++s) {
+            const uint64_t m = part_m[s];
+            if ((m >> lane) & 1) {
+              const int qi = lane + 64 * s;
+              const int rank = P + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+              uint16_t* e = lst + (rank >> 1) * 8 + (rank & 1);
+              e[0] = (uint16_t)qx[s];
+              e[2] = (uint16_t)qy[s];
+              e[4] = (uint16_t)(s_T[qi * F + abs(qf[s] - fmin)] + 1);
+              e[6] = (uint16_t)(s_T[qi * F + abs(qf[s] - fmax)] + 1);
+            }
+            P += popc(m);
+          }
+          if ((P & 1) && lane == 0) {
+            // pad the last pair with a query that covers nothing (T + 1 = 0)
+            uint16_t* e = lst + (P >> 1) * 8 + 1;
+            e[0] = 0;
+            e[2] = 0;
+            e[4] = 0;
+            e[6] = 0;
+          }
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          short2_t kxx[QPL], kyy[QPL];
+          ushort2_t cp[QPL];
+          int tf[QPL];
+#pragma unroll
+          for (int s = 0; s < QPL; ++s) {
+            kxx[s] = (short2_t){(short)kx[s], (short)kx[s]};
+            kyy[s] = (short2_t){(short)ky[s], (short)ky[s]};
+            cp[s] = (ushort2_t){0, 0};
+            tf[s] = kf[s] == fmin ? 2 : 3;
+          }
+          const int pairs = (P + 1) >> 1;
+          for (int k = 0; k < pairs; ++k) {
+            const uint32_t* ent = &s_pairs[wave][k][0];
+            const short2_t X = __builtin_bit_cast(short2_t, ent[0]);
+            const short2_t Y = __builtin_bit_cast(short2_t, ent[1]);
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+              const short2_t T1 = __builtin_bit_cast(short2_t, ent[tf[s]]);
+              const short2_t dx = kxx[s] - X, dy = kyy[s] - Y;
+              const short2_t diff = dx * dx + dy * dy - T1;
+              cp[s] += __builtin_bit_cast(ushort2_t, diff) >> (unsigned short)15;
+            }
+            if (RULE == TRA_MASK_UNION) {
+              bool hit = false;
+#pragma unroll
+              for (int s = 0; s < QPL; ++s) hit |= kvalid[s] && (cp[s][0] | cp[s][1]) != 0;
+              if (ballot(hit) != 0) break;  // one covered key decides the union
+            }
+          }
+#pragma unroll
+          for (int s = 0; s < QPL; ++s) c[s] += (int)cp[s][0] + (int)cp[s][1];
+        } else if (fmax - fmin <= 1) {
           // Block v spans at most two frames, so a query needs two thresholds
           // here: ta for keys of frame fmin, tb for keys of frame fmax.  The
           // partial queries are then walked with their data broadcast from
@@ -319,7 +393,8 @@ template <int B, int RULE, int DIST>
 void launch_mask_variant(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask, int32_t* cnt,
                          int32_t* cols, hipStream_t s) {
   const int32_t* thr = DIST == TRA_DIST_1D ? p.d_thr1 : p.d_thr;
-  hipLaunchKernelGGL((block_mask_kernel<B, RULE, DIST>), dim3(p.rows), dim3(256), 0, s, radius_sq, p.d_perm,
+  const size_t lds = (size_t)B * p.cfg.frames * sizeof(int32_t);
+  hipLaunchKernelGGL((block_mask_kernel<B, RULE, DIST>), dim3(p.rows), dim3(256), lds, s, radius_sq, p.d_perm,
                      p.d_coord, thr, p.d_blocks, mask, cnt, cols, p.N, p.S, p.NB, p.cfg.frames,
                      p.cfg.height, p.cfg.width, p.n_cap);
 }
