@@ -4,8 +4,8 @@
 // online-softmax entropy pass (App. C.2, Alg. 2).  Three kernels:
 //   attn_k64_kernel   dense and block-sparse output, 64-key tiles, three
 //                     4-wave workgroups per CU;
-//   attn_bf16_kernel  token-level output and the entropy pass, 128-key tiles,
-//                     two 4-wave workgroups per CU;
+//   attn_bf16_kernel  token-level output (two 4-wave workgroups per CU) and the
+//                     entropy pass (four), 128-key tiles;
 //   attn_fused_kernel the entropy pass fused with the dense output, 8 waves
 //                     splitting the keys of one query block.
 //
@@ -19,12 +19,13 @@
 //   permutation inside the kernel, so callers keep raster order.
 //
 // Work decomposition
-//   One workgroup (4 waves, 256 threads) per query-block row r = (b, h, u):
-//   128 queries, wave w owning queries [32w, 32w + 32).  It walks the key
-//   blocks of its row (all NB for dense; cols[r][0..cnt[r]) for sparse).
-//   Several workgroups share a CU, so a SIMD can run one workgroup's matrix
-//   phase while another is in its softmax: three with 64-key tiles (32 KB of
-//   LDS each), two with 128-key tiles (64 KB each).
+//   The unit of work is a query-block row r = (b, h, u): 128 queries, wave w of
+//   a 4-wave workgroup owning queries [32w, 32w + 32), walking the key blocks
+//   of the row (all NB for dense; cols[r][0..cnt[r]) for sparse).  Every kernel
+//   is persistent: as many workgroups as can be resident, each taking rows
+//   from a row queue (per-XCD contiguous ranges with stealing, see next_row)
+//   until it is drained.  Several workgroups share a CU, so a SIMD can run one
+//   workgroup's matrix phase while another is in its softmax.
 //
 // Per tile (split barriers)
 //   K and V^T go from HBM straight into LDS (global_load_lds_dwordx4 from a
