@@ -214,8 +214,10 @@ tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t
 
 /* Block-sparse attention: a query of block u takes one softmax over every key
  * of the key blocks cols[r][0..cnt[r]) (r its row) and attends to no other key
- * (Eq. 16 at block granularity).  Rows are processed in `order` when it is
- * non-NULL (entries outside [0, rows) are skipped), else in row order.
+ * (Eq. 16 at block granularity).  With a non-NULL `order`, only the rows it
+ * lists are computed, handed out in that order (entries outside [0, rows) are
+ * skipped); with NULL every row is computed.  The schedule never changes a
+ * row's result.
  * cnt values are clamped to [0, NB]; column ids outside [0, NB) are skipped.
  * o: output; lse: fp32 natural-log log-sum-exp of the scaled scores over the
  * retained keys, or NULL.  A row with cnt = 0 gets o = 0, lse = -inf. */

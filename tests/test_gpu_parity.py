@@ -316,6 +316,51 @@ def test_row_schedule_does_not_change_results(name):
             assert bool((got == 7.0).all()), r
 
 
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny"])
+def test_empty_rows_give_zero_output(name):
+    """A row whose list is empty (cnt = 0, or only out-of-range ids) has no key
+    to attend to: its queries get o = 0 and lse = -inf, as the header states;
+    every other row is bitwise the normal call's."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    run = Run(SMALL[name])
+    NB = run.plan.n_blocks
+    rows = run.plan.rows
+    cnt, cols = run.cnt.cpu().numpy().copy(), run.cols.cpu().numpy().copy()
+    flat_c, flat_l = cnt.reshape(-1), cols.reshape(rows, NB)
+    empty = np.arange(0, rows, 3)
+    flat_c[empty[::2]] = 0
+    flat_l[empty[1::2], :] = -1            # non-zero count, but no valid id
+    dev = run.q.device
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    o, l = torch.empty_like(run.O_sp), torch.empty_like(run.lse_sp)
+    tra.tra_sparse_attention(run.plan, run.q, run.k, run.v, t(cnt), t(cols), None, o, l)
+    torch.cuda.synchronize()
+    perm_tok = OracleTables(run.w).perm
+    S = o.shape[2]
+    blk = np.arange(S) // run.w.block
+    for r in range(rows):
+        bh, u = divmod(r, NB)
+        b, h = divmod(bh, o.shape[1])
+        toks = perm_tok[blk == u]
+        if r in set(empty.tolist()):
+            assert bool((o[b, h, toks] == 0).all()), r
+            assert bool(torch.isneginf(l[b, h, toks]).all()), r
+        else:
+            assert torch.equal(o[b, h, toks], run.O_sp[b, h, toks]), r
+            assert torch.equal(l[b, h, toks], run.lse_sp[b, h, toks]), r
+    # the token-level call (same lists) follows the same rule
+    ot, lt = torch.empty_like(o), torch.empty_like(l)
+    tra.tra_token_attention(run.plan, run.q, run.k, run.v, run.rad, t(cnt), t(cols), None, ot, lt)
+    torch.cuda.synchronize()
+    for r in empty.tolist():
+        bh, u = divmod(r, NB)
+        b, h = divmod(bh, o.shape[1])
+        toks = perm_tok[blk == u]
+        assert bool((ot[b, h, toks] == 0).all()) and bool(torch.isneginf(lt[b, h, toks]).all()), r
+
+
 def test_determinism_bitwise():
     _gpu()
     import torch
