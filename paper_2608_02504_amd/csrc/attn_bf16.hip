@@ -649,6 +649,8 @@ __device__ __forceinline__ void bf16_row(
   using G = Geo<D>;
   uint16_t* thrq = (uint16_t*)(smemCols + ((NB + 3) & ~3));
   const int bh = r / NB, u = r - bh * NB;
+  // (opaque: the lane arithmetic below is redone per row instead of being
+  // hoisted out of the persistent row loop, where it would stay live and spill)
   const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int col = lane & 31, half = lane >> 5;
@@ -942,6 +944,8 @@ __device__ __forceinline__ void k64_row(
   constexpr int KT_BYTES = kKT * D * 2;            // one 64-key tile of K or V^T
   constexpr int STEPS = KT_BYTES / 4096;           // 4 KB copy steps per tile
   const int bh = r / NB, u = r - bh * NB;
+  // (opaque: the lane arithmetic below is redone per row instead of being
+  // hoisted out of the persistent row loop, where it would stay live and spill)
   const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int col = lane & 31, half = lane >> 5;
@@ -1202,6 +1206,8 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
   constexpr int GROUP_BYTES = 2 * TILE;  // K tile, then V^T tile
   constexpr int KS = TileCopy<D>::STEPS;
   const int bh = r / NB, u = r - bh * NB;
+  // (opaque: the lane arithmetic below is redone per row instead of being
+  // hoisted out of the persistent row loop, where it would stay live and spill)
   const int t = (int)opaque(threadIdx.x), lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int g = wave >> 2, w4 = wave & 3;
