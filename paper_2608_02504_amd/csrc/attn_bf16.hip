@@ -1147,9 +1147,9 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // Grid of a persistent attention kernel: as many workgroups as can be resident
 // at once (the occupancy its registers and LDS allow), capped by the row count.
 template <typename K>
-int resident_grid(K kernel, size_t lds_bytes, const tra_plan_s& p) {
+int resident_grid(K kernel, size_t lds_bytes, const tra_plan_s& p, int threads = kThreads) {
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_bytes) != hipSuccess || per_cu < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, lds_bytes) != hipSuccess || per_cu < 1)
     per_cu = 1;
   return std::min(p.rows, per_cu * std::max(p.n_cu, 1));
 }
@@ -1394,11 +1394,7 @@ __global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
 template <int D>
 void launch_fused_entropy_output(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_fused_kernel<D>, kFusedThreads, 0) != hipSuccess ||
-      per_cu < 1)
-    per_cu = 1;
-  const int grid = std::min(p.rows, per_cu * std::max(p.n_cu, 1));
+  const int grid = resident_grid(attn_fused_kernel<D>, 0, p, kFusedThreads);
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   hipLaunchKernelGGL((attn_fused_kernel<D>), dim3(grid), dim3(kFusedThreads), 0, s, (const uint16_t*)a.q,
                      p.d_kt, p.d_vt, (uint16_t*)a.o, a.entropy, p.d_perm, p.S, p.n_pad, p.NB, p.rows,
