@@ -400,7 +400,7 @@ __device__ __forceinline__ int4v lds_read_i4(const lds_u8* base, uint32_t off) {
 // 16-bit dot product), or |i - j| of raster indices for the 1-D ablation.
 template <int TOK>
 __device__ __forceinline__ int token_metric(int qw, int kw) {
-  if constexpr (TOK == 2) {
+  if constexpr ((TOK & 3) == 2) {
     return abs(qw - kw);
   } else {
     const short2_t d = __builtin_bit_cast(short2_t, qw) - __builtin_bit_cast(short2_t, kw);
@@ -414,15 +414,17 @@ __device__ __forceinline__ int token_metric(int qw, int kw) {
 // the key's frame: t_lo for the block's first frame, t_hi for its second) or
 // the key is a text token, else gets the same large negative score as the
 // ragged tail.  kinfo: the block's 128 key words (distance word, second-frame
-// flag at bit 15 for 2-D / 30 for 1-D, text flag at bit 31).  One code path for
+// flag at bit 15 for 2-D / 30 for 1-D, text flag at bit 31; the text test is
+// compiled in only for plans with text tokens, TOK & 4).  One code path for
 // every block: a second, single-frame specialisation would not fit the
 // kernel's registers alongside it.
 template <int TOK>
 __device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restrict__ kinfo, int half,
                                            int qw, int t_lo, int t_hi) {
   const uint32_t neg = __float_as_uint(-1.0e30f);
-  constexpr int kFrameBit = TOK == 2 ? 30 : 15;
-  constexpr uint32_t kWordMask = TOK == 2 ? 0x3FFFFFFFu : 0x7FFF7FFFu;
+  constexpr int kFrameBit = (TOK & 3) == 2 ? 30 : 15;
+  constexpr uint32_t kWordMask = (TOK & 3) == 2 ? 0x3FFFFFFFu : 0x7FFF7FFFu;
+  constexpr bool kText = (TOK & 4) != 0;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -434,7 +436,7 @@ __device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restr
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int dist = token_metric<TOK>(qw, (int)((uint32_t)w[j] & kWordMask));
-          const bool keep = w[j] < 0 || dist <= (((w[j] >> kFrameBit) & 1) ? t_hi : t_lo);
+          const bool keep = (kText && w[j] < 0) || dist <= (((w[j] >> kFrameBit) & 1) ? t_hi : t_lo);
           const int e = 8 * g + 4 * h4 + j;
           s[kt][e] = keep ? s[kt][e] : __uint_as_float(neg);
         }
@@ -692,7 +694,7 @@ __device__ __forceinline__ void bf16_row(
       n = max(n, 0);
       const int32_t c = tk.coord[qpos];
       tq_f = coord_f(c);
-      tq_word = TOK == 2 ? qrow : (coord_x(c) | (coord_y(c) << 16));
+      tq_word = (TOK & 3) == 2 ? qrow : (coord_x(c) | (coord_y(c) << 16));
       if (!tq_all)
         for (int d = half; d < tk.F; d += 2) thrq[qi * tk.F + d] = (uint16_t)tk.thr[(size_t)n * tk.F + d];
     }
@@ -775,7 +777,7 @@ __device__ __forceinline__ void bf16_row(
           t_lo = thrq[qi * tk.F + abs(tq_f - fmin)];
           t_hi = thrq[qi * tk.F + abs(tq_f - fmax)];
           int dmin, dmax;
-          if constexpr (TOK == 2) {
+          if constexpr ((TOK & 3) == 2) {
             const int rmin = bi[7], rmax = bi[8];
             dmin = max(0, max(rmin - tq_word, tq_word - rmax));
             dmax = max(tq_word - rmin, rmax - tq_word);
@@ -876,7 +878,8 @@ __device__ __forceinline__ void bf16_row(
 }
 
 // TOK (sparse only): 0 block granular; 1 token mask with the 2-D distance,
-// 2 with the 1-D sequence distance (Eq. 15 inside the listed blocks).
+// 2 with the 1-D sequence distance (Eq. 15 inside the listed blocks); + 4 when
+// the plan has text tokens (text keys stay visible).
 // Persistent: as many workgroups as can be resident, each taking rows from the
 // row queue until it is drained (the first barrier of every row, after its list
 // is staged, orders the next s_row write after every wave's read).
@@ -1430,7 +1433,10 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (a.sparse && a.radius_sq && p.cfg.distance == TRA_DIST_1D) launch_variant<D, true, true, false, 2>(p, a, s);
+  const bool text = p.S > p.N;
+  if (a.sparse && a.radius_sq && p.cfg.distance == TRA_DIST_1D && text) launch_variant<D, true, true, false, 6>(p, a, s);
+  else if (a.sparse && a.radius_sq && p.cfg.distance == TRA_DIST_1D) launch_variant<D, true, true, false, 2>(p, a, s);
+  else if (a.sparse && a.radius_sq && text) launch_variant<D, true, true, false, 5>(p, a, s);
   else if (a.sparse && a.radius_sq) launch_variant<D, true, true, false, 1>(p, a, s);
   else if (a.sparse) launch_k64<D, true>(p, a, s);
   else if (a.entropy && a.o) launch_fused_entropy_output<D>(p, a, s);
