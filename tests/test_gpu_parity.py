@@ -397,7 +397,9 @@ def test_wan13b_480p_sampled():
 
 @pytest.mark.slow
 def test_wan14b_720p_sampled():
-    _sampled("wan14b_720p")
+    # sparse attention without a row order, as bench.py times it (the other
+    # large shapes run it with the heaviest-first order)
+    _sampled("wan14b_720p", with_order=False)
 
 
 @pytest.mark.slow
