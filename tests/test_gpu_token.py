@@ -9,7 +9,7 @@ import pytest
 
 import oracle as O
 import synth
-from _pipeline import TOL_O_BF16, TOL_O_FP32, OracleTables, Run, log
+from _pipeline import TOL_O_BF16, TOL_O_FP32, OracleTables, Run, log, sample_blocks
 
 pytestmark = pytest.mark.gpu
 
@@ -164,3 +164,33 @@ def test_token_unsupported_shapes_are_rejected():
         cols = torch.zeros(1, 1, NB, NB, dtype=torch.int32, device="cuda")
         with pytest.raises(tra.TraError, match="UNSUPPORTED"):
             tra.tra_token_attention(plan, x, x, x, rad, cnt, cols, None, torch.empty_like(x))
+
+
+@pytest.mark.slow
+def test_token_attention_720p_sampled_at_paper_density():
+    """Token-level attention at the headline shape with about 15 % of the blocks
+    kept (one constant entropy ln(7997 / tau) for every token), without a row
+    order as the benchmark runs it: 8 sampled query blocks in each of 4 heads
+    against the oracle's token_attention_rows, outputs and lse."""
+    _gpu()
+    w = synth.workload("wan14b_720p")
+    run = Run(w, with_order=False, entropy_override=float(np.log(7997 / w.tau)))
+    o, lse = _token_call(run)
+    tabs = OracleTables(w)
+    worst = 0.0
+    for (b, h), blocks in sample_blocks(w, 8, seed=7).items():
+        if h not in (0, 13, 26, 39):
+            continue
+        q, k, v = (synth.to_f64(a[b, h], w.dtype) for a in (run.q_np, run.k_np, run.v_np))
+        M = run.mask[b, h].cpu().numpy().astype(bool)[blocks]
+        n_tok = run.rad[b, h].cpu().numpy()
+        rows, o_ref, lse_ref = O.token_attention_rows(
+            q, k, v, tabs.perm, w.block, list(blocks), M, n_tok, tabs.F, tabs.H, tabs.W, w.gamma,
+            distance=run.cfg.distance, return_lse=True)
+        err = np.abs(o[b, h].double().cpu().numpy()[rows] - o_ref).max()
+        assert err <= TOL_O_BF16, f"token attention max-abs {err:.3e} (b={b}, h={h})"
+        lse_gpu = lse[b, h].double().cpu().numpy()[rows]
+        assert np.abs(lse_gpu - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "token lse"
+        worst = max(worst, float(err))
+        log(f"wan14b_720p token-level: batch {b} head {h} checked")
+    log(f"wan14b_720p token-level at the paper's density: max-abs {worst:.2e}")
