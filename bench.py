@@ -303,7 +303,7 @@ def joint_driver(tra, w, iters=3):
     return res
 
 
-def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100, target_rho=None):
+def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100, target_rho=None, on_step=None):
     """Warm-up reuse sequence: step 0 from the generator, later steps drift
     q, k <- q, k + 0.02 N(0,1) (fp32 masters, re-rounded).  Every `refresh`
     steps the fused entropy + dense output pass, budget/radius and mask are
@@ -316,7 +316,12 @@ def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100, target_rho=None):
     drift is trivially 0.  With a target, every entropy is lowered by one
     constant (searched at step 0 so the first mask keeps about that fraction)
     before the budget stage, on refresh and fresh masks alike, so the masks
-    are partial and can drift."""
+    are partial and can drift.
+
+    on_step(t, kind, state): called untimed after each step, kind "refresh" or
+    "reuse"; state maps names to the live device tensors (q, k, v, o, the
+    shifted entropy H and radii rad of the step's own inputs, the cached
+    mask / cnt / cols, and on reuse steps the fresh mask fmask) and "shift"."""
     import torch
 
     import synth
@@ -399,6 +404,11 @@ def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100, target_rho=None):
             inter = (m0 & m1).sum().item()
             union = (m0 | m1).sum().item()
             drift.append(((m0 ^ m1).float().mean().item(), 1.0 - inter / max(union, 1)))
+        if on_step is not None:
+            st = dict(q=q, k=k, v=v, o=o, H=H, rad=rad, mask=mask, cnt=cnt, cols=cols, shift=shift)
+            if t % refresh:
+                st["fmask"] = fmask
+            on_step(t, "refresh" if t % refresh == 0 else "reuse", st)
     rho = kept(mask)
     total = sum(refresh_ms) + sum(reuse_ms)
     return {
