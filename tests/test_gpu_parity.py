@@ -395,16 +395,21 @@ def test_wan13b_480p_sampled():
     _sampled("wan13b_480p")
 
 
+# The two 720p shapes compute every head on the GPU; the oracle checks sampled
+# query blocks of an evenly spread subset of heads, which keeps each test's
+# host-side check under a minute (about 4 s per head at 75,600 tokens, 6.5 s at
+# 118,800).  The headline shape's two tests check disjoint head subsets.
+
 @pytest.mark.slow
 def test_wan14b_720p_sampled():
     # sparse attention without a row order, as bench.py times it (the other
     # large shapes run it with the heaviest-first order)
-    _sampled("wan14b_720p", with_order=False)
+    _sampled("wan14b_720p", heads=range(2, 40, 5), with_order=False)
 
 
 @pytest.mark.slow
 def test_hunyuan_720p_sampled():
-    _sampled("hunyuan_720p")
+    _sampled("hunyuan_720p", heads=range(1, 24, 4))
 
 
 @pytest.mark.slow
