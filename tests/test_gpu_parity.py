@@ -40,7 +40,16 @@ SMALL = {
                                    0.25, 4.0, 0.6, seed=81, tile_h=8, tile_w=16),
     "fp32_b64_d128": synth.Workload("fp32_b64_d128", 1, 1, 128, "fp32", 2, 9, 11, 64,
                                     0.25, 4.0, 0.6, seed=82, tile_h=8, tile_w=8),
+    # 45-token frames: each 128-token block spans three or four frames, which the
+    # mask builder's two-frame packed pair test does not cover
+    "small_frames_bf16": synth.Workload("small_frames_bf16", 1, 2, 64, "bf16", 7, 5, 9, 128,
+                                        0.25, 4.0, 0.6, seed=83, tile_h=8, tile_w=16),
 }
+
+# 90 x 160 frames: n_cap = 89^2 + 159^2 = 33,202, beyond the range of the mask
+# builder's 16-bit packed distances, so every pair takes the 32-bit test.
+WIDE = synth.Workload("wide_frame_bf16", 1, 1, 64, "bf16", 2, 90, 160, 128,
+                      0.25, 4.0, 0.6, seed=84, tile_h=8, tile_w=16)
 
 
 @pytest.mark.parametrize("name", list(SMALL))
@@ -135,7 +144,7 @@ def test_joint_zero_radius(name):
 
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128",
-                                  "joint_bf16_d128"])
+                                  "joint_bf16_d128", "small_frames_bf16"])
 @pytest.mark.parametrize("radius", [3, 40, 250])
 @pytest.mark.parametrize("rule,distance", [("vote", "2d"), ("union", "2d"), ("vote", "1d")])
 def test_mid_radius_masks_exact(name, radius, rule, distance):
@@ -155,6 +164,41 @@ def test_mid_radius_masks_exact(name, radius, rule, distance):
             M_ref = O.block_mask_rows(n_full[b, h], tabs.perm, w.block, tabs.F, tabs.H, tabs.W,
                                       w.gamma, list(range(w.n_blocks)), rule=rule, distance=distance)
             assert np.array_equal(mask[b, h], M_ref), (b, h, np.nonzero((mask[b, h] != M_ref).any(1))[0][:5])
+    check_lists(run)
+
+
+@pytest.mark.parametrize("budget", [1500, 6000])
+def test_wide_frame_sampled(budget):
+    """Every stage on sampled query blocks of the 90 x 160 grid, with one constant
+    entropy ln(budget / tau) for every token: the radius bisection runs over
+    [0, 33,202] and the block masks are partial."""
+    _gpu()
+    w = WIDE
+    tabs = OracleTables(w)
+    assert tabs.ncap >= 32767
+    run = Run(w, with_order=False, entropy_override=float(np.log(budget / w.tau)))
+    report = {}
+    for (b, h), blocks in sample_blocks(w, 16, seed=5).items():
+        check_head(run, tabs, b, h, blocks, TOL_O_BF16, report)
+    check_lists(run)
+    rho = retained_fraction(run)
+    log(f"{w.name} budget {budget}: rho={rho:.4f} {report}")
+    assert 0.0 < rho < 0.9
+
+
+def test_wide_frame_mask_exact():
+    """A partially covering radius (n = 2,000) on the 90 x 160 grid: every mask
+    row equals the oracle's Alg. 1."""
+    _gpu()
+    w = WIDE
+    run = Run(w, radius_override=2000)
+    tabs = OracleTables(w)
+    n_full = run.rad.cpu().numpy()
+    mask = run.mask.cpu().numpy().astype(bool)
+    M_ref = O.block_mask_rows(n_full[0, 0], tabs.perm, w.block, tabs.F, tabs.H, tabs.W, w.gamma,
+                              list(range(w.n_blocks)))
+    assert np.array_equal(mask[0, 0], M_ref), np.nonzero((mask[0, 0] != M_ref).any(1))[0][:5]
+    assert 0.05 < M_ref.mean() < 0.95
     check_lists(run)
 
 
