@@ -44,6 +44,13 @@ SMALL = {
     # mask builder's two-frame packed pair test does not cover
     "small_frames_bf16": synth.Workload("small_frames_bf16", 1, 2, 64, "bf16", 7, 5, 9, 128,
                                         0.25, 4.0, 0.6, seed=83, tile_h=8, tile_w=16),
+    # the largest frame count a plan accepts (64): per-query thresholds for 64
+    # frame distances, blocks spanning four 32-token frames
+    "max_frames_bf16": synth.Workload("max_frames_bf16", 1, 1, 128, "bf16", 64, 4, 8, 128,
+                                      0.25, 4.0, 0.6, seed=85, tile_h=8, tile_w=16),
+    # a single frame: only the frame distance 0 exists
+    "one_frame_bf16": synth.Workload("one_frame_bf16", 1, 2, 128, "bf16", 1, 30, 52, 128,
+                                     0.25, 4.0, 0.6, seed=86, tile_h=8, tile_w=16),
 }
 
 # 90 x 160 frames: n_cap = 89^2 + 159^2 = 33,202, beyond the range of the mask
@@ -144,7 +151,8 @@ def test_joint_zero_radius(name):
 
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128",
-                                  "joint_bf16_d128", "small_frames_bf16"])
+                                  "joint_bf16_d128", "small_frames_bf16", "max_frames_bf16",
+                                  "one_frame_bf16"])
 @pytest.mark.parametrize("radius", [3, 40, 250])
 @pytest.mark.parametrize("rule,distance", [("vote", "2d"), ("union", "2d"), ("vote", "1d")])
 def test_mid_radius_masks_exact(name, radius, rule, distance):
