@@ -58,6 +58,11 @@ SMALL = {
 WIDE = synth.Workload("wide_frame_bf16", 1, 1, 64, "bf16", 2, 90, 160, 128,
                       0.25, 4.0, 0.6, seed=84, tile_h=8, tile_w=16)
 
+# Close to the largest block count a plan accepts (4,096 per head): 63 frames of
+# 90 x 92 = 521,640 tokens, 4,076 blocks, the last one ragged (40 tokens).
+MAXB = synth.Workload("max_blocks_bf16", 1, 1, 64, "bf16", 63, 90, 92, 128,
+                      0.25, 4.0, 0.6, seed=87, tile_h=8, tile_w=16)
+
 
 @pytest.mark.parametrize("name", list(SMALL))
 def test_small_full_parity(name):
@@ -191,6 +196,26 @@ def test_wide_frame_sampled(budget):
     check_lists(run)
     rho = retained_fraction(run)
     log(f"{w.name} budget {budget}: rho={rho:.4f} {report}")
+    assert 0.0 < rho < 0.9
+
+
+@pytest.mark.slow
+def test_max_blocks_sampled():
+    """Every stage on sampled query blocks (the ragged last among them) of a
+    4,076-block sequence, with a uniform budget of 20,000 keys (partial masks)
+    and the heaviest-first row order: block lists, the row-order histogram and
+    the sparse kernel's staged list at nearly their largest."""
+    _gpu()
+    w = MAXB
+    assert w.n_blocks == 4076 and w.n_tokens % w.block == 40
+    tabs = OracleTables(w)
+    run = Run(w, entropy_override=float(np.log(20000 / w.tau)))
+    report = {}
+    for (b, h), blocks in sample_blocks(w, 4, seed=9).items():
+        check_head(run, tabs, b, h, blocks, TOL_O_BF16, report)
+    check_lists(run)
+    rho = retained_fraction(run)
+    log(f"{w.name}: rho={rho:.4f} {report}")
     assert 0.0 < rho < 0.9
 
 
