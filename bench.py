@@ -212,7 +212,7 @@ def _time_sparse(tra, plan, q, k, v, cnt, cols, o, iters):
 
 def mask_variants(tra, w, q, k, v, H, dense_ms, iters=3, tag=""):
     """The plan's budget-mapping and distance options on the headline inputs,
-    from the same entropies: the lognormal mapping (App. B) and the
+    from the same entropies: the lognormal mapping (App. A.2) and the
     sequence-distance ablation (App. C.1), each with its budget/radius + mask
     time, retained fraction and sparse attention time."""
     import torch

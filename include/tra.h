@@ -8,7 +8,7 @@
  *                         Alg. 2), optionally fused with the dense output O.
  *   tra_budget_radius     entropy -> budget K_hat = ceil(tau * exp(H))
  *                         (Sec. 3.1, Eq. 8; or the entropy-identified
- *                         lognormal mapping of App. B) -> smallest
+ *                         lognormal mapping of App. A.2) -> smallest
  *                         boundary-aware squared radius reaching it
  *                         (Sec. 3.2, Eqs. 13-14).
  *   tra_build_block_mask  per-token radii -> Boolean query-block x key-block
@@ -99,7 +99,7 @@ typedef enum { TRA_MASK_VOTE = 0, TRA_MASK_UNION = 1 } tra_mask_rule;
 
 /* Entropy-to-budget mapping.  UNIFORM is the paper's K_hat = ceil(tau e^H)
  * (Sec. 3.1, Eq. 8).  LOGNORMAL is the entropy-identified lognormal mapping of
- * App. B: with S keys per attention row, sigma = sqrt(2 (log S - H)) and
+ * App. A.2: with S keys per attention row, sigma = sqrt(2 (log S - H)) and
  * K_hat = ceil(S * Phibar(sigma - Phi^{-1}(tau))), Phibar = 1 - Phi the
  * standard normal tail; at H = log S both give ceil(tau S). */
 typedef enum { TRA_BUDGET_UNIFORM = 0, TRA_BUDGET_LOGNORMAL = 1 } tra_budget_map;

@@ -35,7 +35,7 @@ RADIUS_FULL = 2 ** 31 - 1
 __all__ = [
     "RADIUS_FULL", "grid_coords", "tile_major_order", "block_bounds",
     "scores", "softmax_rows", "dense_attention", "entropy_from_probs",
-    "entropy_online", "token_budget", "n_cap", "threshold_table",
+    "entropy_from_scores", "token_budget", "n_cap", "threshold_table",
     "within_radius", "grid_count_bruteforce", "disk_count_table", "grid_count",
     "select_radius", "select_radius_linear", "token_mask_rows",
     "block_mask_rows", "masked_attention_rows", "retained_fraction",
@@ -119,40 +119,12 @@ def entropy_from_probs(p) -> np.ndarray:
     return (-(p * torch.log(safe)).sum(dim=1)).numpy()
 
 
-def entropy_online(q, k, v, kv_tile: int):
-    """Alg. 2 (App. C.2): online softmax with one extra running sum.
-
-    Per query row: m = -inf, l = 0, a = 0, o = 0; for each KV tile r:
-    s = alpha q K_r^T, m_r = max s, w = exp(s - m_r), l_r = sum w,
-    a_r = sum w s, o_r = sum w v; m' = max(m, m_r); u = exp(m - m');
-    v' = exp(m_r - m'); l = u l + v' l_r; a = u a + v' a_r; o = u o + v' o_r;
-    m = m'.  Finally O = o / l and H = log l + m - a / l, which is the identity
-    H = log Z - sum_j p_ij s_ij of App. C.2.
-    Returns (O, H) for all rows of q.
-    """
-    q, k, v = _t(q), _t(k), _t(v)
-    R, d = q.shape
-    alpha = 1.0 / math.sqrt(d)
-    m = torch.full((R,), -math.inf, dtype=torch.float64)
-    l = torch.zeros(R, dtype=torch.float64)
-    a = torch.zeros(R, dtype=torch.float64)
-    o = torch.zeros(R, v.shape[1], dtype=torch.float64)
-    for s0 in range(0, k.shape[0], kv_tile):
-        kr, vr = k[s0:s0 + kv_tile], v[s0:s0 + kv_tile]
-        s = alpha * (q @ kr.T)
-        m_r = s.max(dim=1).values
-        w = torch.exp(s - m_r[:, None])
-        l_r = w.sum(dim=1)
-        a_r = (w * s).sum(dim=1)
-        o_r = w @ vr
-        m_new = torch.maximum(m, m_r)
-        u = torch.exp(m - m_new)
-        vv = torch.exp(m_r - m_new)
-        l = u * l + vv * l_r
-        a = u * a + vv * a_r
-        o = u[:, None] * o + vv[:, None] * o_r
-        m = m_new
-    return (o / l[:, None]).numpy(), (torch.log(l) + m - a / l).numpy()
+def entropy_from_scores(q, k):
+    """H_i = log Z_i - sum_j p_ij s_ij over whole rows (the identity behind the
+    fused entropy kernel, App. C.2), fp64: log Z by logsumexp, p by softmax."""
+    s = scores(q, k)
+    p = softmax_rows(s)
+    return (torch.logsumexp(s, dim=1) - (p * s).sum(dim=1)).numpy()
 
 
 # ====================================================== entropy -> budget
@@ -178,7 +150,7 @@ def normal_tail(z):
 
 def lognormal_top_mass(q, sigma):
     """L_LN(q) = Phibar(Phi^{-1}(1 - q) - sigma): the expected share of the total
-    held by the largest fraction q of Lognormal(mu, sigma^2) samples (App. B,
+    held by the largest fraction q of Lognormal(mu, sigma^2) samples (App. A.2,
     "Entropy-identified Lognormal mapping")."""
     q = np.asarray(q, dtype=np.float64)
     zq = np.vectorize(lambda a: NormalDist().inv_cdf(a))(1.0 - q)
@@ -186,7 +158,7 @@ def lognormal_top_mass(q, sigma):
 
 
 def token_budget_lognormal(H, tau: float, S: int) -> np.ndarray:
-    """Lognormal entropy-to-budget mapping (App. B): the weights of a row of S
+    """Lognormal entropy-to-budget mapping (App. A.2): the weights of a row of S
     keys are modelled as Lognormal(mu, sigma^2); entropy fixes
     sigma = sqrt(2 (log S - H)) (H = log S - sigma^2 / 2), and the retained
     fraction solving L_LN(q) = tau is B = Phibar(sigma - Phi^{-1}(tau)).  The key

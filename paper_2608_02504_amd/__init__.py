@@ -75,7 +75,7 @@ class Config:
     rule: str = "vote"        # "vote" (Alg. 1) or "union"
     tau: float = 0.9
     gamma: float = 0.6
-    budget: str = "uniform"   # "uniform" (Eq. 8) or "lognormal" (App. B)
+    budget: str = "uniform"   # "uniform" (Eq. 8) or "lognormal" (App. A.2)
     distance: str = "2d"      # "2d" (Eq. 15) or "1d" (sequence-distance ablation)
     text_tokens: int = 0      # text tokens after the video tokens (joint attention)
 

@@ -1,7 +1,7 @@
 // Entropy -> budget -> squared radius, one thread per (batch, head, token).
 //
 //  K_hat = ceil(tau * exp(H))                       Sec. 3.1, Eq. 8 (fp64)
-//    or, lognormal mapping (App. B, Eq. lognormal_budget_appendix), with S keys
+//    or, lognormal mapping (App. A.2, Eq. lognormal_budget_appendix), with S keys
 //    per row: K_hat = ceil(S * Phibar(sqrt(2 (log S - H)) - Phi^{-1}(tau)))
 //  C(n)  = sum_t #{(x', y') in frame : (x-x')^2 + (y-y')^2 <= thr[n][|t-f|]}
 //                                                   Sec. 3.2, Eq. 13

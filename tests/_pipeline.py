@@ -166,7 +166,7 @@ def check_head(run: Run, tabs: OracleTables, b: int, h: int, blocks, tol_o: floa
     report["max_err_fused"] = max(report.get("max_err_fused", 0.0), float(erre))
 
     # budget and radius from the GPU's fp32 entropy (Eqs. 8, 13, 14, or the
-    # lognormal mapping of App. B): bit-exact for video tokens; text tokens
+    # lognormal mapping of App. A.2): bit-exact for video tokens; text tokens
     # carry budget S and the FULL radius
     Nv = w.n_video
     video = rows < Nv

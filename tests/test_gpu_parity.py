@@ -103,7 +103,7 @@ def _full_check(run, report):
 
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "ragged_bf16_d64", "tiny", "fp32_b64_d128"])
 def test_lognormal_budget_parity(name):
-    """App. B lognormal mapping: budgets (fp64 on both sides, ties at an integer
+    """App. A.2 lognormal mapping: budgets (fp64 on both sides, ties at an integer
     allowed one apart), radii, masks and outputs against the oracle."""
     _gpu()
     run = Run(SMALL[name], budget="lognormal")

@@ -38,8 +38,7 @@ def test_two_key_closed_form():
     assert np.allclose(o, [[3.0, 0.0]], atol=1e-14)
     H = O.entropy_from_probs(p)
     assert abs(H[0] - (math.log(4) - 0.75 * math.log(3))) < 1e-14
-    o2, H2 = O.entropy_online(q, k, v, kv_tile=1)
-    assert np.allclose(o2, [[3.0, 0.0]], atol=1e-14)
+    H2 = O.entropy_from_scores(q, k)
     assert abs(H2[0] - (math.log(4) - 0.75 * math.log(3))) < 1e-14
 
 
@@ -55,7 +54,7 @@ def test_uniform_scores_give_log_n(N):
     H = O.entropy_from_probs(p)
     assert np.allclose(H, math.log(N), atol=1e-12)
     assert np.allclose(o, v.mean(axis=0), atol=1e-12)
-    _, H2 = O.entropy_online(q, k, v, kv_tile=64)
+    H2 = O.entropy_from_scores(q, k)
     assert np.allclose(H2, math.log(N), atol=1e-12)
 
 
@@ -71,7 +70,7 @@ def test_one_hot_scores_give_zero_entropy():
     H = O.entropy_from_probs(p)
     assert 0.0 <= H[0] < N * math.exp(-40) * 41
     assert np.allclose(o[0], v[17], atol=1e-12)
-    _, H2 = O.entropy_online(q, k, v, kv_tile=32)
+    H2 = O.entropy_from_scores(q, k)
     assert abs(H2[0]) < 1e-9
 
 
@@ -106,18 +105,15 @@ def test_lognormal_scores_entropy():
 
 def test_entropy_bounds_and_two_forms_agree():
     """0 <= H <= log N (Eq. 2), and the direct -sum p log p agrees with the
-    online Alg. 2 accumulation H = log l + m - a/l to 1e-12 for every KV tile
-    size."""
+    identity H = log Z - sum_j p_j s_j (App. C.2) to 1e-12."""
     w = synth.workload("tiny")
     q, k, v = synth.generate(w)
     q, k, v = (synth.to_f64(a[0, 1], w.dtype) for a in (q, k, v))
     o, p = O.dense_attention(q, k, v, return_probs=True)
     H = O.entropy_from_probs(p)
     assert (H >= 0).all() and (H <= math.log(256) + 1e-12).all()
-    for tile in (1, 17, 64, 256):
-        o2, H2 = O.entropy_online(q, k, v, tile)
-        assert np.abs(H2 - H).max() < 1e-12
-        assert np.abs(o2 - o).max() < 1e-12
+    H2 = O.entropy_from_scores(q, k)
+    assert np.abs(H2 - H).max() < 1e-12
 
 
 def test_attention_key_permutation_invariance():
@@ -400,7 +396,7 @@ def test_masked_attention_lse_is_log_partition():
     assert np.abs(lse - np.log(np.exp(s).sum(axis=1))).max() < 1e-12
 
 
-# ------------------------------------------------------- lognormal budget (App. B)
+# ------------------------------------------------------- lognormal budget (App. A.2)
 @pytest.mark.parametrize("S", [256, 32760, 75600, 119056])
 def test_lognormal_budget_at_max_entropy_is_tau_s(S):
     """At H = log S the fitted sigma is 0 (equal weights), Phibar(-Phi^{-1}(tau))
@@ -415,7 +411,7 @@ def test_lognormal_budget_at_max_entropy_is_tau_s(S):
 
 
 def test_lognormal_budget_inverts_top_mass():
-    """B = Phibar(sigma - Phi^{-1}(tau)) solves L_LN(B) = tau (App. B): with
+    """B = Phibar(sigma - Phi^{-1}(tau)) solves L_LN(B) = tau (App. A.2): with
     Phi^{-1}(1 - B) = sigma - Phi^{-1}(tau), L_LN(B) = Phibar(-Phi^{-1}(tau))."""
     z = O.normal_quantile(0.9)
     for sigma in (0.0, 0.3, 1.0, 2.5, 4.0):
