@@ -28,3 +28,25 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stderr
+
+
+def test_kept_fraction_matches_executed_flops():
+    """The device-side count the benchmark uses (run here on CPU tensors) equals
+    the host count, and its fraction is over 4 d N^2 per (batch, head)."""
+    import torch
+    rng = np.random.default_rng(4)
+    for N, b, d in ((1000, 128, 128), (75600, 128, 128)):
+        nb = -(-N // b)
+        mask = rng.random((1, 2, nb, nb)) < 0.3
+        rho, fl = bench.kept_fraction(torch.from_numpy(mask.astype(np.uint8)), N, b, d)
+        assert fl == bench.executed_flops(mask, N, b, d)
+        assert abs(rho - fl / (4.0 * d * N * N * 2)) < 1e-15
+
+
+def test_mask_source_adjusts_entropies():
+    """own leaves H alone, entropy subtracts its constant, uniform overwrites H."""
+    import torch
+    H = torch.tensor([1.0, 2.5, 7.0])
+    assert torch.equal(bench.MaskSource("own").apply(H.clone()), H)
+    assert torch.equal(bench.MaskSource("entropy", 1.5).apply(H.clone()), H - 1.5)
+    assert torch.equal(bench.MaskSource("uniform", 3.0).apply(H.clone()), torch.full_like(H, 3.0))

@@ -1,8 +1,10 @@
 """The warm-up reuse sequence (Sec. 3.3) against the oracle, step by step.
 
-A short drifting sequence runs through the benchmark's reuse driver on a
-reduced 480p grid (5 x 30 x 52 = 7,800 tokens, a ragged last block), with the
-entropies shifted so that the masks keep about 30 % of the blocks.  After every
+Drifting sequences run through the benchmark's reuse driver: a short one on a
+reduced 480p grid (5 x 30 x 52 = 7,800 tokens, a ragged last block) with the
+entropies shifted so that the masks keep about 30 % of the blocks, every step
+checked; and the 50-step sequence at its own shape (21 x 30 x 52, 12 heads),
+sampled query blocks of every head checked on selected steps.  After a checked
 step the test checks, on the host:
 
 * refresh step: the fused pass's dense output (Eq. 2) and entropy (Eq. 1) of
@@ -18,8 +20,8 @@ import pytest
 
 import oracle as O
 import synth
-from _pipeline import (TOL_H_ABS, TOL_H_REL, TOL_O_BF16, OracleTables, log, sample_blocks,
-                       to_np_f64)
+from _pipeline import (TOL_H_ABS, TOL_H_REL, TOL_O_BF16, OracleTables, dense_reference, log,
+                       sample_blocks, to_np_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -42,72 +44,114 @@ def _check_lists(mask, cnt, cols):
         assert (c2[r, n2[r]:] == -1).all()
 
 
-def test_reuse_sequence_steps_match_oracle():
-    _gpu()
+def _run_sequence(w, steps, target_rho, blocks_per_head, check_steps=None, full_masks=False):
+    """Runs the benchmark's reuse driver on `w` and checks, after each step in
+    `check_steps` (every step when None), the sampled query blocks of every head
+    against the oracle; on every other step only that the cached lists are
+    unchanged.  full_masks: compare whole mask arrays (small grids), else the
+    mask rows of the sampled blocks."""
     import bench
     import torch
     import paper_2608_02504_amd as tra
-    w = W
     tabs = OracleTables(w)
     N, b, NB = w.n_tokens, w.block, w.n_blocks
-    assert N % b != 0                                   # ragged last block
-    blocks = sample_blocks(w, 4, seed=11)
-    all_blocks = list(range(NB))
+    blocks = sample_blocks(w, blocks_per_head, seed=11)
     seen = {"refresh": 0, "reuse": 0}
     cached = {}
     host_drift = []
     q0 = {}
 
-    def mask_ref(rad, h):
-        return O.block_mask_rows(rad[0, h], tabs.perm, b, tabs.F, tabs.H, tabs.W, w.gamma, all_blocks)
+    def mask_ref(rad, h, sel):
+        return O.block_mask_rows(rad[0, h], tabs.perm, b, tabs.F, tabs.H, tabs.W, w.gamma, sel)
+
+    def mask_check(mask, rad, h, what):
+        sel = list(range(NB)) if full_masks else list(blocks[(0, h)])
+        assert np.array_equal(mask[0, h][sel], mask_ref(rad, h, sel)), f"{what} head {h}"
 
     def on_step(t, kind, st):
         seen[kind] += 1
+        if kind == "refresh":
+            cached.update(mask=st["mask"].clone(), cnt=st["cnt"].clone(), cols=st["cols"].clone())
+        else:
+            assert torch.equal(st["mask"], cached["mask"]), f"step {t}: cached mask changed"
+            assert torch.equal(st["cnt"], cached["cnt"]) and torch.equal(st["cols"], cached["cols"]), \
+                f"step {t}: cached lists changed"
+            host_drift.append(float((cached["mask"] ^ st["fmask"]).float().mean()))
+        if check_steps is not None and t not in check_steps:
+            return
         q, k, v = (to_np_f64(st[n]) for n in ("q", "k", "v"))
         o = to_np_f64(st["o"])
         mask = st["mask"].cpu().numpy().astype(bool)
-        cnt, cols = st["cnt"].cpu().numpy(), st["cols"].cpu().numpy()
         rad = st["rad"].cpu().numpy()
         if t == 0:
-            q0["q"] = q
-        elif t == 1:
-            assert not np.array_equal(q, q0["q"]), "q does not drift between steps"
+            q0["q"] = q[0, 0, :64].copy()
+        elif "q" in q0:
+            assert not np.array_equal(q[0, 0, :64], q0["q"]), "q does not drift between steps"
         err = 0.0
         if kind == "refresh":
             H = st["H"].double().cpu().numpy() + st["shift"]
             for h in range(w.heads):
                 rows = np.concatenate([tabs.perm[u * b:min((u + 1) * b, N)] for u in blocks[(0, h)]])
-                p = O.softmax_rows(O.scores(q[0, h][rows], k[0, h]))
-                H_ref = O.entropy_from_probs(p)
-                O_ref = (p @ torch.as_tensor(v[0, h])).numpy()
+                H_ref, O_ref, _ = dense_reference(q[0, h], k[0, h], v[0, h], rows)
                 dH = np.abs(H[0, h][rows] - H_ref)
                 assert (dH <= np.maximum(TOL_H_REL * np.abs(H_ref), TOL_H_ABS) + 1e-6 * st["shift"]).all(), \
                     f"step {t} head {h}: entropy max |dH| {dH.max():.3e}"
                 err = max(err, float(np.abs(o[0, h][rows] - O_ref).max()))
-                assert np.array_equal(mask[0, h], mask_ref(rad, h)), f"step {t} head {h}: refresh mask"
-            _check_lists(mask, cnt, cols)
-            cached.update(mask=mask, cnt=cnt, cols=cols)
+                mask_check(mask, rad, h, f"step {t}: refresh mask")
+            _check_lists(mask, st["cnt"].cpu().numpy(), st["cols"].cpu().numpy())
         else:
-            assert np.array_equal(mask, cached["mask"]), f"step {t}: cached mask changed"
-            assert np.array_equal(cnt, cached["cnt"]) and np.array_equal(cols, cached["cols"]), \
-                f"step {t}: cached lists changed"
             fmask = st["fmask"].cpu().numpy().astype(bool)
             for h in range(w.heads):
                 sel = list(blocks[(0, h)])
                 rows, O_ref = O.masked_attention_rows(q[0, h], k[0, h], v[0, h], tabs.perm, b, sel,
-                                                      cached["mask"][0, h][sel])
+                                                      mask[0, h][sel])
                 err = max(err, float(np.abs(o[0, h][rows] - O_ref).max()))
-                assert np.array_equal(fmask[0, h], mask_ref(rad, h)), f"step {t} head {h}: fresh mask"
-            host_drift.append(float((cached["mask"] ^ fmask).mean()))
+                mask_check(fmask, rad, h, f"step {t}: fresh mask")
         assert err <= TOL_O_BF16, f"step {t} ({kind}): output max-abs {err:.3e}"
         log(f"step {t} {kind}: output max-abs {err:.3e}, kept {mask.mean():.3f} of the blocks")
 
-    res = bench.reuse_driver(tra, w, steps=7, refresh=5, target_rho=0.3, on_step=on_step)
-    assert seen == {"refresh": 2, "reuse": 5}
+    res = bench.reuse_driver(tra, w, steps=steps, refresh=5, target_rho=target_rho, on_step=on_step)
+    n_ref = (steps + 4) // 5
+    assert seen == {"refresh": n_ref, "reuse": steps - n_ref}
+    assert res["refresh_step_ms"] > 0 and res["reuse_step_ms"] > 0
+    assert res["mask_drift_hamming_mean"] == pytest.approx(np.mean(host_drift), rel=1e-6, abs=1e-9)
+    assert res["mask_drift_hamming_max"] == pytest.approx(np.max(host_drift), rel=1e-6, abs=1e-9)
+    log(f"reuse sequence: {res}")
+    return res, host_drift
+
+
+def test_reuse_sequence_steps_match_oracle():
+    """Reduced grid, every step checked, whole masks compared."""
+    _gpu()
+    w = W
+    assert w.n_tokens % w.block != 0                                   # ragged last block
+    res, host_drift = _run_sequence(w, 7, 0.3, 4, full_masks=True)
     assert res["entropy_shift_nats"] > 0
     assert 0.05 < res["retained_fraction_last_mask"] < 0.9, res["retained_fraction_last_mask"]
     assert max(host_drift) > 0                          # the fresh masks do differ from the cached ones
-    assert res["mask_drift_hamming_mean"] == pytest.approx(np.mean(host_drift), rel=1e-6, abs=1e-9)
-    assert res["mask_drift_hamming_max"] == pytest.approx(np.max(host_drift), rel=1e-6, abs=1e-9)
-    assert res["refresh_step_ms"] > 0 and res["reuse_step_ms"] > 0
-    log(f"reuse sequence: {res}")
+
+
+@pytest.mark.slow
+def test_reuse_480p_full_sequence_at_paper_density():
+    """The warm-up reuse workload at its own shape (21 x 30 x 52, 12 heads, 50
+    steps, refresh every 5) with the entropies shifted to keep ~15 % of the
+    blocks, as the benchmark runs it: 32 sampled query blocks of every head are
+    checked on three refresh steps (the first, a middle one and the last) and two
+    reuse steps (the first and the last);
+    every reuse step keeps the cached lists."""
+    _gpu()
+    w = synth.workload("reuse_480p")
+    res, host_drift = _run_sequence(w, 50, 0.15, 32, check_steps={0, 1, 25, 45, 49})
+    assert res["entropy_shift_nats"] > 0
+    assert 0.1 < res["retained_fraction_last_mask"] < 0.2, res["retained_fraction_last_mask"]
+
+
+@pytest.mark.slow
+def test_reuse_480p_full_sequence():
+    """The same sequence with the workload's own entropies (every block kept,
+    so no drift): sampled blocks of every head on one refresh and one reuse
+    step."""
+    _gpu()
+    w = synth.workload("reuse_480p")
+    res, host_drift = _run_sequence(w, 50, None, 32, check_steps={0, 1})
+    assert res["entropy_shift_nats"] == 0
