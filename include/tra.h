@@ -220,7 +220,17 @@ tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t
  * row's result.
  * cnt values are clamped to [0, NB]; column ids outside [0, NB) are skipped.
  * o: output; lse: fp32 natural-log log-sum-exp of the scaled scores over the
- * retained keys, or NULL.  A row with cnt = 0 gets o = 0, lse = -inf. */
+ * retained keys, or NULL.  A row with cnt = 0 gets o = 0, lse = -inf.
+ * Work is balanced by cutting long lists: with T the total of the (clamped)
+ * list lengths of the rows computed and G the number of workgroups the GPU
+ * holds at once, a row of more than L = max(48, ceil(T / 16G)) entries (L
+ * doubled while the pieces would not fit the plan's 256 MiB partial workspace)
+ * is computed as ceil(cnt / L) pieces of consecutive entries whose partial
+ * softmax states are merged afterwards, so its result differs from an
+ * unsplit computation by rounding only (each piece rounds its probabilities
+ * to bf16 relative to its own running maximum); rows of at most 48 entries
+ * are never split.  The output is normalised by the sum of the
+ * bf16-rounded probabilities that multiply V (lse by the fp32 sum). */
 tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
                                 const void* v, const int32_t* cnt, const int32_t* cols,
                                 const int32_t* order, void* o, float* lse, void* stream);

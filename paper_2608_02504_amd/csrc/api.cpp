@@ -1,5 +1,6 @@
 // C ABI entry points of the TRA library: argument checks, plan lifetime,
 // dispatch to the kernel launchers.  No exception leaves this file.
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -107,11 +108,17 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_thr);
   (void)hipFree(p->d_thr1);
   (void)hipFree(p->d_blocks);
+  (void)hipFree(p->d_cap_count);
   (void)hipFree(p->d_sort_ws);
   (void)hipFree(p->d_kt);
   (void)hipFree(p->d_vt);
   (void)hipFree(p->d_kinfo);
   (void)hipFree(p->d_row_ctr);
+  (void)hipFree(p->d_units);
+  (void)hipFree(p->d_splits);
+  (void)hipFree(p->d_unit_hdr);
+  (void)hipFree(p->d_part);
+  (void)hipFree(p->d_pstats);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -169,6 +176,12 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
     }
+    if ((e = hipMalloc((void**)&p->d_cap_count, (size_t)std::max(p->N, 1) * sizeof(int32_t))) != hipSuccess ||
+        (e = tra::fill_cap_counts(*p, p->d_cap_count, nullptr)) != hipSuccess ||
+        (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
+      tra_plan_destroy(p);
+      return fail(TRA_ERR_ALLOC, std::string("plan count table: ") + hipGetErrorString(e));
+    }
     if (cfg->dtype == TRA_BF16) {
       const size_t bytes = (size_t)cfg->batch * cfg->heads * p->n_pad * cfg->head_dim * sizeof(uint16_t);
       if ((e = hipMalloc((void**)&p->d_kt, bytes)) != hipSuccess ||
@@ -177,6 +190,18 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
           (e = hipMalloc((void**)&p->d_row_ctr, tra::kRowCounters * sizeof(int32_t))) != hipSuccess) {
         tra_plan_destroy(p);
         return fail(TRA_ERR_ALLOC, std::string("plan K/V workspace: ") + hipGetErrorString(e));
+      }
+      p->split_wg_cap = tra::k64_sparse_grid_cap(*p);
+      tra::split_capacities(p->split_wg_cap, p->rows, cfg->head_dim, &p->units_cap, &p->splits_cap,
+                           &p->slots_cap);
+      const size_t slot_floats = (size_t)128 * cfg->head_dim;
+      if ((e = hipMalloc((void**)&p->d_units, (size_t)p->units_cap * 4 * sizeof(int32_t))) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_splits, (size_t)p->splits_cap * 4 * sizeof(int32_t))) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_unit_hdr, 4 * sizeof(int32_t))) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_part, (size_t)p->slots_cap * slot_floats * sizeof(float))) != hipSuccess ||
+          (e = hipMalloc((void**)&p->d_pstats, (size_t)p->slots_cap * 3 * 128 * sizeof(float))) != hipSuccess) {
+        tra_plan_destroy(p);
+        return fail(TRA_ERR_ALLOC, std::string("plan work-unit tables: ") + hipGetErrorString(e));
       }
     }
     *out = p;

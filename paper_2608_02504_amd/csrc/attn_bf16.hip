@@ -304,9 +304,19 @@ __device__ __forceinline__ void mask_tail(f32x16 (&s)[4], int nv, int half) {
     }
 }
 
+// lr is the sum of the weights as rounded to the bf16 probabilities that PV
+// multiplies (the output is normalised by it, so that the bf16 weights form an
+// exact convex combination: a query dominated by one key gets that key's value
+// to fp32 rounding); l is the fp32 sum (log-sum-exp, entropy).
 struct RowState {
-  float m, l, a;  // running max (log2 units), sum of weights, entropy sum
+  float m, l, a, lr;  // running max (log2 units), sum of weights, entropy sum, rounded sum
 };
+
+// acc + the two bf16 probabilities packed in p, in fp32 (one v_dot2 with 1.0).
+__device__ __forceinline__ float add_bf16_pair(uint32_t p, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), __builtin_bit_cast(bf16x2, 0x3F803F80u),
+                                         acc, false);
+}
 
 // Floor of the running max (log2 units), far below any real score and far
 // above the masked ones (-1e30 times the scale): a tile whose keys are all
@@ -343,25 +353,34 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;
+  st.lr *= sc;
   st.m = m_new;
   return sc;
 }
 
 // Weights of sub-tile kt: w = 2^(s alpha log2e - m), summed into l (and w x into
 // a); bf16 pairs into pb[8kt .. 8kt+7].
-template <bool PV, bool ENT>
+// With PV the rounded pairs are also summed into lrsum (four independent
+// accumulation chains: one long chain of dot products would stall the wave on
+// their latency); with LF the fp32 weights into lsum.
+template <bool PV, bool ENT, bool LF = true>
 __device__ __forceinline__ void tile_exp(const f32x16& s, float scale_log2, float m, float& lsum,
-                                         float& asum, uint32_t* pb) {
+                                         float& asum, float& lrsum, uint32_t* pb) {
+  float lr4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int e = 0; e < 16; e += 2) {
     const float x0 = fmaf(s[e], scale_log2, -m);
     const float x1 = fmaf(s[e + 1], scale_log2, -m);
     const float w0 = __builtin_amdgcn_exp2f(x0);
     const float w1 = __builtin_amdgcn_exp2f(x1);
-    lsum += w0 + w1;
+    if (LF) lsum += w0 + w1;
     if (ENT) asum = fmaf(w0, x0, fmaf(w1, x1, asum));
-    if (PV) pb[e >> 1] = pack_bf16x2(w0, w1);
+    if (PV) {
+      pb[e >> 1] = pack_bf16x2(w0, w1);
+      lr4[(e >> 1) & 3] = add_bf16_pair(pb[e >> 1], lr4[(e >> 1) & 3]);
+    }
   }
+  if (PV) lrsum += (lr4[0] + lr4[1]) + (lr4[2] + lr4[3]);
 }
 
 // O^T += V^T P^T.  k-step ks covers keys [16ks, 16ks+16); in lane half h the
@@ -502,6 +521,7 @@ __device__ __forceinline__ float tile_max_tree(const f32x16 (&s)[4], float scale
   const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
   if (ENT) st.a = st.l > 0.f ? sc * (st.a + st.l * (st.m - m_new)) : 0.f;
   st.l *= sc;
+  st.lr *= sc;
   st.m = m_new;
   return sc;
 }
@@ -605,7 +625,8 @@ __device__ __forceinline__ void pv_tile_copies(f32x16 (&oacc)[Geo<D>::D_TILES], 
 // exponentials run.  C counts the copy steps issued so far.
 template <int D, bool PV, bool ENT, int P0, int PEND, int NC, int P = P0>
 __device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, float (&lp)[4], float (&ap)[4],
-                                          uint32_t* pb, uint32_t lds, const uint8_t* src, uint32_t off) {
+                                          float (&lr)[4], uint32_t* pb, uint32_t lds, const uint8_t* src,
+                                          uint32_t off) {
   if constexpr (P < PEND) {
     constexpr int kt = P / 8, e = (P % 8) * 2;
     const float x0 = fmaf(s[kt][e], c, -m);
@@ -614,7 +635,10 @@ __device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, floa
     const float w1 = __builtin_amdgcn_exp2f(x1);
     lp[kt] += w0 + w1;
     if (ENT) ap[kt] = fmaf(w0, x0, fmaf(w1, x1, ap[kt]));
-    if (PV) pb[P] = pack_bf16x2(w0, w1);
+    if (PV) {
+      pb[P] = pack_bf16x2(w0, w1);
+      lr[kt] = add_bf16_pair(pb[P], lr[kt]);
+    }
     // copies [C, C_NEXT) follow this pair: ceil(NC (pairs done) / pairs in range)
     constexpr int C = ((P - P0) * NC + (PEND - P0) - 1) / (PEND - P0);
     constexpr int C_NEXT = ((P + 1 - P0) * NC + (PEND - P0) - 1) / (PEND - P0);
@@ -630,7 +654,7 @@ __device__ __forceinline__ void exp_pairs(f32x16 (&s)[4], float c, float m, floa
         lp[kt] = nxt;
       }
     }
-    exp_pairs<D, PV, ENT, P0, PEND, NC, P + 1>(s, c, m, lp, ap, pb, lds, src, off);
+    exp_pairs<D, PV, ENT, P0, PEND, NC, P + 1>(s, c, m, lp, ap, lr, pb, lds, src, off);
   }
 }
 
@@ -737,7 +761,7 @@ __device__ __forceinline__ void bf16_row(
   for (int i = 0; i < (PV ? G::D_TILES : 1); ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
-  RowState st{-INFINITY, 0.f, 0.f};
+  RowState st{-INFINITY, 0.f, 0.f, 0.f};
 
   // token variant: wave 0 copies each tile's key info (1 KB) right after its
   // K steps, into the buffer of the tile's parity, so "K landed" covers it
@@ -812,12 +836,13 @@ __device__ __forceinline__ void bf16_row(
         }
         if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
         sc = tile_max<ENT>(s, scale_log2, st);
-        float lsum = 0.f, asum = 0.f;
+        float lsum = 0.f, asum = 0.f, lrsum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
-          tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
+          tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
         }
         st.l += lsum;
+        if (PV) st.lr += lrsum;
         if (ENT) st.a += asum;
       }
       if constexpr (PV) {
@@ -855,10 +880,11 @@ __device__ __forceinline__ void bf16_row(
 
   const float l_tot = sum_halves(st.l);
   const float a_tot = ENT ? sum_halves(st.a) : 0.f;
+  const float lr_tot = PV ? sum_halves(st.lr) : 0.f;
   if (!qvalid) return;
   const size_t tok = (size_t)bh * N + qrow;
   if (PV) {
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float inv = lr_tot > 0.f ? 1.f / lr_tot : 0.f;
     uint16_t* dst = o + tok * D;
 #pragma unroll
     for (int dt = 0; dt < G::D_TILES; ++dt)
@@ -936,13 +962,19 @@ __device__ __forceinline__ void issue_steps_strided(uint32_t lds_wave, const uin
   }
 }
 
-template <int D, bool SPARSE>
+// One work unit of a row: list positions [beg, end) of row r (the whole row
+// for dense).  slot < 0: the unit is the whole row and writes the normalised
+// output (and lse).  slot >= 0: one piece of a split row; it writes its
+// unnormalised output, running max and sums to partial slot `slot` for the
+// merge kernel.  LSE: also keep the fp32 sum of the weights for the
+// log-sum-exp output.
+template <int D, bool SPARSE, bool LSE>
 __device__ __forceinline__ void k64_row(
-    int r, uint8_t* smemK, uint8_t* smemV, int32_t* smemCols,
+    int r, int beg, int end, int slot, uint8_t* smemK, uint8_t* smemV, int32_t* smemCols,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
     uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, int N,
-    int n_pad, int NB, float scale_log2) {
+    const int32_t* __restrict__ cols, int N, int n_pad, int NB, float scale_log2,
+    float* __restrict__ part, float* __restrict__ pstats) {
   using G = Geo<D>;
   constexpr int KT_BYTES = kKT * D * 2;            // one 64-key tile of K or V^T
   constexpr int STEPS = KT_BYTES / 4096;           // 4 KB copy steps per tile
@@ -973,9 +1005,9 @@ __device__ __forceinline__ void k64_row(
       qf[kk] = __builtin_bit_cast(bf16x8, x);
     }
   }
-  const int count = SPARSE ? min(max(cnt[r], 0), NB) : NB;
+  const int count = SPARSE ? end - beg : NB;
   if constexpr (SPARSE) {
-    const int32_t* colp = cols + (size_t)r * NB;
+    const int32_t* colp = cols + (size_t)r * NB + beg;
     for (int j = t; j < count; j += kThreads) smemCols[j] = colp[j];
   }
   wait_vm<0>();
@@ -1009,7 +1041,7 @@ __device__ __forceinline__ void k64_row(
   for (int i = 0; i < G::D_TILES; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
-  RowState st{-INFINITY, 0.f, 0.f};
+  RowState st{-INFINITY, 0.f, 0.f, 0.f};
 
   int pos;
   int bt_cur = next_valid(0, &pos);
@@ -1059,13 +1091,16 @@ __device__ __forceinline__ void k64_row(
       mx = max_halves(mx);
       const float m_new = next_reference(st.m, mx * scale_log2);
       const float sc = __builtin_amdgcn_exp2f(st.m - m_new);
-      st.l *= sc;
+      if (LSE) st.l *= sc;
+      st.lr *= sc;
       st.m = m_new;
       uint32_t pb[16];
-      float lsum = 0.f, asum = 0.f;
+      float lsum = 0.f, asum = 0.f, lrsum = 0.f;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) tile_exp<true, false>(s[kt], scale_log2, st.m, lsum, asum, pb + 8 * kt);
-      st.l += lsum;
+      for (int kt = 0; kt < 2; ++kt)
+        tile_exp<true, false, LSE>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+      if (LSE) st.l += lsum;
+      st.lr += lrsum;
       if (has_next) wait_vm<STEPS>();  // V^T landed (the next K tile may still be in flight)
       else wait_vm<0>();
       lds_barrier();
@@ -1099,10 +1134,29 @@ __device__ __forceinline__ void k64_row(
     }
   }
 
-  const float l_tot = sum_halves(st.l);
+  const float lr_tot = sum_halves(st.lr);
+  const float l_tot = LSE ? sum_halves(st.l) : 0.f;
+  if (SPARSE && slot >= 0) {
+    // a piece of a split row: O relative to 2^m, unnormalised, [slot][query][D]
+    const int qi = wave * 32 + col;
+    float* po = part + ((size_t)slot * kBQ + qi) * D;
+#pragma unroll
+    for (int dt = 0; dt < G::D_TILES; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *(float4*)(po + dt * 32 + 8 * g + 4 * half) =
+            make_float4(oacc[dt][4 * g], oacc[dt][4 * g + 1], oacc[dt][4 * g + 2], oacc[dt][4 * g + 3]);
+    if (half == 0) {
+      float* ps = pstats + (size_t)slot * 3 * kBQ;
+      ps[qi] = st.m;
+      ps[kBQ + qi] = lr_tot;
+      ps[2 * kBQ + qi] = l_tot;
+    }
+    return;
+  }
   if (!qvalid) return;
   const size_t tok = (size_t)bh * N + qrow;
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float inv = lr_tot > 0.f ? 1.f / lr_tot : 0.f;
   uint16_t* dst = o + tok * D;
 #pragma unroll
   for (int dt = 0; dt < G::D_TILES; ++dt)
@@ -1114,36 +1168,244 @@ __device__ __forceinline__ void k64_row(
       w.y = pack_bf16x2(oacc[dt][4 * g + 2] * inv, oacc[dt][4 * g + 3] * inv);
       *(uint2*)(dst + d0) = w;
     }
-  if (half == 0 && lse) lse[tok] = l_tot > 0.f ? 0.69314718055994531f * (st.m + __log2f(l_tot)) : -INFINITY;
+  if (LSE && half == 0) lse[tok] = l_tot > 0.f ? 0.69314718055994531f * (st.m + __log2f(l_tot)) : -INFINITY;
+}
+
+// Queue of work units (thread 0 of a workgroup only): with `single`, one
+// counter walks the units in table order (the caller's row order); otherwise
+// per-XCD contiguous ranges with stealing, as next_row.  Returns -1 once all
+// is drained.
+__device__ __forceinline__ int next_unit(int32_t* ctr, bool single, int n, int xcd, int& steal) {
+  if (single) {
+    const int k = atomicAdd(&ctr[0], 1);
+    return k < n ? k : -1;
+  }
+  const int per = n / 8, rem = n % 8;
+  while (steal < 8) {
+    const int qd = (xcd + steal) & 7;
+    const int beg = qd * per + min(qd, rem), cnt = per + (qd < rem ? 1 : 0);
+    const int k = atomicAdd(&ctr[qd * 16], 1);
+    if (k < cnt) return beg + k;
+    ++steal;
+  }
+  return -1;
 }
 
 // Persistent kernel: as many workgroups as fit on the GPU (three per CU), each
-// taking rows from the row queue until it is drained.  Every row starts with a
-// workgroup barrier (after its block list is staged), which also orders the
-// next s_row write after every wave's read of the current one.
-template <int D, bool SPARSE>
+// taking work from a queue until it is drained: rows (dense), or the units of
+// the work-unit table (block-sparse; see plan_units_kernel).  Every unit starts
+// with a workgroup barrier (after its block list is staged), which also orders
+// the next s_row write after every wave's read of the current one.
+template <int D, bool SPARSE, bool LSE>
 __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
     uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ cnt, const int32_t* __restrict__ cols, const int32_t* __restrict__ order, int N,
-    int n_pad, int NB, int rows, float scale_log2, int32_t* __restrict__ ctr) {
+    const int32_t* __restrict__ cols, const int4* __restrict__ units, const int32_t* __restrict__ unit_hdr,
+    bool ordered, int N, int n_pad, int NB, int rows, float scale_log2, int32_t* __restrict__ ctr,
+    float* __restrict__ part, float* __restrict__ pstats) {
   constexpr int KT_BYTES = kKT * D * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t smemK[KT_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t smemV[KT_BYTES];
   extern __shared__ int32_t smemCols[];
   __shared__ int s_row, s_steal;  // thread 0's queue state lives in LDS, not in a register
+  const int n_work = SPARSE ? unit_hdr[0] : rows;
   if (threadIdx.x == 0) s_steal = 0;
   for (;;) {
     if (threadIdx.x == 0) {
       int steal = s_steal;
-      s_row = next_row(ctr, SPARSE ? order : nullptr, rows, blockIdx.x & 7, steal);
+      s_row = SPARSE ? next_unit(ctr, ordered, n_work, blockIdx.x & 7, steal)
+                     : next_row(ctr, nullptr, rows, blockIdx.x & 7, steal);
       s_steal = steal;
     }
     __syncthreads();
-    const int r = s_row;
-    if (r < 0) break;
-    k64_row<D, SPARSE>(r, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cnt, cols, N, n_pad, NB,
-                       scale_log2);
+    const int w = s_row;
+    if (w < 0) break;
+    if constexpr (SPARSE) {
+      const int4 un = units[w];
+      if (un.x < 0) {  // a placeholder unit (never written by a consistent plan): nothing to do
+        __syncthreads();
+        continue;
+      }
+      k64_row<D, true, LSE>(un.x, un.y, un.z, un.w, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cols,
+                            N, n_pad, NB, scale_log2, part, pstats);
+    } else {
+      k64_row<D, false, LSE>(w, 0, NB, -1, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cols, N, n_pad,
+                             NB, scale_log2, part, pstats);
+    }
+  }
+}
+
+// Work units of a block-sparse call (one workgroup of 1024 threads).  The row
+// lists are walked in the caller's order (or row order); with T the total
+// list length and G the attention grid, L = max(kSplitMin, ceil(T / (G
+// kSplitPerWG))), doubled until the pieces fit the plan's partial slots, and a
+// row of c > L entries becomes ceil(c / L) units of near-equal length, each
+// writing a partial slot, so that no unit holds more than about
+// 1 / kSplitPerWG of a workgroup's share of the work and the rows the call
+// waits on at its end are short, while short rows are never cut into pieces
+// whose fixed costs (query load, partial write, merge) would dominate.  Rows of
+// at most L entries are one unit each (and give the same result as an unsplit
+// call).  Writes units[U] = {row, list begin, list end, slot or -1},
+// splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L}.  A split row
+// has c / L < pieces < 2 c / L, so P <= T / L <= G kSplitPerWG and
+// U <= rows + G kSplitPerWG: the plan sizes its tables by these bounds
+// (entries past a capacity are never written).
+constexpr int kSplitPerWG = 16;
+constexpr long long kSplitSlotBytes = 256ll << 20;  // partial workspace of a plan
+constexpr int kSplitMin = 48;
+
+__global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restrict__ cnt,
+                                                          const int32_t* __restrict__ order, int rows, int NB,
+                                                          int n_wg, int4* __restrict__ units, int units_cap,
+                                                          int4* __restrict__ splits, int splits_cap,
+                                                          int slots_cap, int32_t* __restrict__ hdr) {
+  __shared__ long long s_red[1024];
+  __shared__ int s_scan[3][1024];
+  const int t = threadIdx.x;
+  const int per = (rows + 1023) / 1024;
+  const int k0 = min(rows, t * per), k1 = min(rows, k0 + per);
+  auto row_at = [&](int k) { return order ? order[k] : k; };
+  auto len_of = [&](int r) { return (r >= 0 && r < rows) ? min(max(cnt[r], 0), NB) : -1; };
+  long long tot = 0;
+  for (int k = k0; k < k1; ++k) tot += max(len_of(row_at(k)), 0);
+  s_red[t] = tot;
+  __syncthreads();
+  for (int st = 512; st > 0; st >>= 1) {
+    if (t < st) s_red[t] += s_red[t + st];
+    __syncthreads();
+  }
+  const long long total = s_red[0];
+  const long long share = (long long)max(n_wg, 1) * kSplitPerWG;
+  int L = (int)max((long long)kSplitMin, (total + share - 1) / share);
+  // per thread: units, slots and split rows of its positions; L doubles until
+  // the pieces of the split rows fit the partial slots
+  int nu, ns, np;
+  for (;;) {
+    nu = ns = np = 0;
+    for (int k = k0; k < k1; ++k) {
+      const int c = len_of(row_at(k));
+      if (c < 0) continue;
+      const int pieces = c > L ? (c + L - 1) / L : 1;
+      nu += pieces;
+      if (pieces > 1) {
+        ns += pieces;
+        ++np;
+      }
+    }
+    __syncthreads();
+    s_red[t] = ns;
+    __syncthreads();
+    for (int st = 512; st > 0; st >>= 1) {
+      if (t < st) s_red[t] += s_red[t + st];
+      __syncthreads();
+    }
+    if (s_red[0] <= slots_cap || L >= NB) break;
+    L = min(2 * L, NB);
+  }
+  s_scan[0][t] = nu;
+  s_scan[1][t] = ns;
+  s_scan[2][t] = np;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive scans
+    int a0 = 0, a1 = 0, a2 = 0;
+    if (t >= off) {
+      a0 = s_scan[0][t - off];
+      a1 = s_scan[1][t - off];
+      a2 = s_scan[2][t - off];
+    }
+    __syncthreads();
+    s_scan[0][t] += a0;
+    s_scan[1][t] += a1;
+    s_scan[2][t] += a2;
+    __syncthreads();
+  }
+  int ub = s_scan[0][t] - nu, sb = s_scan[1][t] - ns, pb = s_scan[2][t] - np;
+  for (int k = k0; k < k1; ++k) {
+    const int r = row_at(k);
+    const int c = len_of(r);
+    if (c < 0) continue;
+    const int pieces = c > L ? (c + L - 1) / L : 1;
+    // (past a capacity -- impossible by the bounds above -- the row stays one
+    // unit and its other entries become placeholders the kernel skips)
+    const bool split = pieces > 1 && sb + pieces <= slots_cap && pb < splits_cap;
+    for (int s = 0; s < pieces; ++s) {
+      const int b0 = (int)((long long)c * s / pieces), b1 = (int)((long long)c * (s + 1) / pieces);
+      int4 un = make_int4(r, b0, b1, split ? sb + s : -1);
+      if (!split && pieces > 1) un = s == 0 ? make_int4(r, 0, c, -1) : make_int4(-1, 0, 0, -1);
+      if (ub + s < units_cap) units[ub + s] = un;
+    }
+    if (split) splits[pb] = make_int4(r, sb, pieces, 0);
+    ub += pieces;
+    if (pieces > 1) {
+      sb += pieces;
+      ++pb;
+    }
+  }
+  if (t == 1023) {
+    hdr[0] = min(s_scan[0][1023], units_cap);
+    hdr[1] = min(s_scan[2][1023], splits_cap);
+    hdr[2] = L;
+  }
+}
+
+// Merges the pieces of the split rows: m = max over pieces of m_p (pieces
+// with no weight skipped), w_p = 2^(m_p - m), o = sum_p w_p O_p / sum_p w_p lr_p
+// (the rounded sums the pieces' bf16 weights add up to), lse = ln 2 (m +
+// log2 sum_p w_p l_p).  One workgroup per split row at a time; thread t takes
+// query t / 2 and half t % 2 of its D outputs.
+template <int D, bool LSE>
+__global__ __launch_bounds__(256) void merge_split_rows_kernel(const int4* __restrict__ splits,
+                                                               const int32_t* __restrict__ hdr,
+                                                               const float* __restrict__ part,
+                                                               const float* __restrict__ pstats,
+                                                               uint16_t* __restrict__ o, float* __restrict__ lse,
+                                                               const int32_t* __restrict__ perm, int N, int NB) {
+  constexpr int HD = D / 2;
+  const int n_split = hdr[1];
+  const int t = threadIdx.x, qi = t >> 1, hd = t & 1;
+  for (int sp = blockIdx.x; sp < n_split; sp += gridDim.x) {
+    const int4 e = splits[sp];
+    const int r = e.x, slot0 = e.y, pieces = e.z;
+    const int bh = r / NB, u = r - bh * NB;
+    const int qpos = u * kBQ + qi;
+    if (qpos >= N) continue;
+    float m = -INFINITY;
+    for (int p = 0; p < pieces; ++p) {
+      const float* ps = pstats + (size_t)(slot0 + p) * 3 * kBQ;
+      if (ps[kBQ + qi] > 0.f) m = fmaxf(m, ps[qi]);
+    }
+    float acc[HD];
+#pragma unroll
+    for (int j = 0; j < HD; ++j) acc[j] = 0.f;
+    float lr = 0.f, lf = 0.f;
+    for (int p = 0; p < pieces; ++p) {
+      const float* ps = pstats + (size_t)(slot0 + p) * 3 * kBQ;
+      const float lrp = ps[kBQ + qi];
+      if (!(lrp > 0.f)) continue;
+      const float w = __builtin_amdgcn_exp2f(ps[qi] - m);
+      lr += w * lrp;
+      if (LSE) lf += w * ps[2 * kBQ + qi];
+      const float4* src = (const float4*)(part + ((size_t)(slot0 + p) * kBQ + qi) * D + hd * HD);
+#pragma unroll
+      for (int j = 0; j < HD / 4; ++j) {
+        const float4 x = src[j];
+        acc[4 * j] += w * x.x;
+        acc[4 * j + 1] += w * x.y;
+        acc[4 * j + 2] += w * x.z;
+        acc[4 * j + 3] += w * x.w;
+      }
+    }
+    const size_t tok = (size_t)bh * N + perm[qpos];
+    const float inv = lr > 0.f ? 1.f / lr : 0.f;
+    uint2* dst = (uint2*)(o + tok * D + hd * HD);
+#pragma unroll
+    for (int j = 0; j < HD / 4; ++j) {
+      uint2 w2;
+      w2.x = pack_bf16x2(acc[4 * j] * inv, acc[4 * j + 1] * inv);
+      w2.y = pack_bf16x2(acc[4 * j + 2] * inv, acc[4 * j + 3] * inv);
+      dst[j] = w2;
+    }
+    if (LSE && hd == 0) lse[tok] = lf > 0.f ? 0.69314718055994531f * (m + __log2f(lf)) : -INFINITY;
   }
 }
 
@@ -1157,15 +1419,44 @@ int resident_grid(K kernel, size_t lds_bytes, const tra_plan_s& p, int threads =
   return std::min(p.rows, per_cu * std::max(p.n_cu, 1));
 }
 
-template <int D, bool SPARSE>
-void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+template <int D>
+int k64_sparse_grid_cap_d(const tra_plan_s& p) {
+  const size_t lds_bytes = (size_t)p.NB * sizeof(int32_t);
+  int a = 0, b = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, attn_k64_kernel<D, true, true>, kThreads, lds_bytes) !=
+      hipSuccess)
+    a = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, attn_k64_kernel<D, true, false>, kThreads, lds_bytes) !=
+      hipSuccess)
+    b = 1;
+  return std::max(1, std::max(a, b)) * std::max(p.n_cu, 1);
+}
+
+template <int D, bool SPARSE, bool LSE>
+void launch_k64_lse(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const size_t lds_bytes = SPARSE ? (size_t)p.NB * sizeof(int32_t) : 0;
-  const int grid = resident_grid(attn_k64_kernel<D, SPARSE>, lds_bytes, p);
+  int grid = resident_grid(attn_k64_kernel<D, SPARSE, LSE>, lds_bytes, p);
+  if (SPARSE) {
+    grid = std::min(grid, p.split_wg_cap);
+    hipLaunchKernelGGL(plan_units_kernel, dim3(1), dim3(1024), 0, s, a.cnt, a.order, p.rows, p.NB, grid,
+                       (int4*)p.d_units, p.units_cap, (int4*)p.d_splits, p.splits_cap, p.slots_cap, p.d_unit_hdr);
+  }
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
-  hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE>), dim3(grid), dim3(kThreads), lds_bytes, s, (const uint16_t*)a.q,
-                     p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB,
-                     p.rows, scale_log2, p.d_row_ctr);
+  hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE, LSE>), dim3(grid), dim3(kThreads), lds_bytes, s,
+                     (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cols,
+                     (const int4*)p.d_units, p.d_unit_hdr, a.order != nullptr, p.S, p.n_pad, p.NB, p.rows,
+                     scale_log2, p.d_row_ctr, p.d_part, p.d_pstats);
+  if (SPARSE)
+    hipLaunchKernelGGL((merge_split_rows_kernel<D, LSE>), dim3(std::max(1, std::min(p.splits_cap, 1024))),
+                       dim3(256), 0, s, (const int4*)p.d_splits, p.d_unit_hdr, p.d_part, p.d_pstats,
+                       (uint16_t*)a.o, a.lse, p.d_perm, p.S, p.NB);
+}
+
+template <int D, bool SPARSE>
+void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
+  if (a.lse) launch_k64_lse<D, SPARSE, true>(p, a, s);
+  else launch_k64_lse<D, SPARSE, false>(p, a, s);
 }
 
 // ------------------------------------------------------------ fused entropy + dense output
@@ -1197,7 +1488,7 @@ void launch_k64(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
 constexpr int kFusedThreads = 512;
 
 // One query-block row r of the fused kernel.  smem: per group a K tile, then a
-// V^T tile; smemState: group 1's (m, l, a) per query, for the merge.
+// V^T tile; smemState: group 1's (m, l, a, lr) per query, for the merge.
 template <int D>
 __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState,
                                           const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile,
@@ -1248,7 +1539,7 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
   for (int i = 0; i < G::D_TILES; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[i][e] = 0.f;
-  RowState st{-INFINITY, 0.f, 0.f};
+  RowState st{-INFINITY, 0.f, 0.f, 0.f};
   uint32_t pb[32];
   f32x16 s[4];
 
@@ -1279,15 +1570,17 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
     // ---- vector phase i
     if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
     const float sc = tile_max_tree<true>(s, scale_log2, st);
-    float lp[4] = {0.f, 0.f, 0.f, 0.f}, ap[4] = {0.f, 0.f, 0.f, 0.f};
+    float lp[4] = {0.f, 0.f, 0.f, 0.f}, ap[4] = {0.f, 0.f, 0.f, 0.f}, lr[4] = {0.f, 0.f, 0.f, 0.f};
     if (has_next)
-      exp_pairs<D, true, true, 0, 16, KS>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb + b_nxt * kTileBytes, k_off);
+      exp_pairs<D, true, true, 0, 16, KS>(s, scale_log2, st.m, lp, ap, lr, pb, k_lds, Kb + b_nxt * kTileBytes,
+                                          k_off);
     else
-      exp_pairs<D, true, true, 0, 16, 0>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb, k_off);
+      exp_pairs<D, true, true, 0, 16, 0>(s, scale_log2, st.m, lp, ap, lr, pb, k_lds, Kb, k_off);
     lds_barrier();
-    exp_pairs<D, true, true, 16, 32, 0>(s, scale_log2, st.m, lp, ap, pb, k_lds, Kb, k_off);
+    exp_pairs<D, true, true, 16, 32, 0>(s, scale_log2, st.m, lp, ap, lr, pb, k_lds, Kb, k_off);
     st.l += (lp[0] + lp[1]) + (lp[2] + lp[3]);
     st.a += (ap[0] + ap[1]) + (ap[2] + ap[3]);
+    st.lr += (lr[0] + lr[1]) + (lr[2] + lr[3]);
     if (__ballot(sc != 1.0f) != 0) {
 #pragma unroll
       for (int dt = 0; dt < G::D_TILES; ++dt)
@@ -1312,6 +1605,7 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
   // vector phase waits for all of them), so group 1's buffers take its O.
   float l_tot = sum_halves(st.l);
   float a_tot = sum_halves(st.a);
+  float lr_tot = sum_halves(st.lr);
   const int qi = w4 * 32 + col;
   if (g == 1) {
     float4* dst = (float4*)(smem + GROUP_BYTES);
@@ -1323,12 +1617,14 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
       smemState[qi] = st.m;
       smemState[kBQ + qi] = l_tot;
       smemState[2 * kBQ + qi] = a_tot;
+      smemState[3 * kBQ + qi] = lr_tot;
     }
   }
   lds_barrier();
   if (g == 1) return;
   {
     const float m1 = smemState[qi], l1 = smemState[kBQ + qi], a1 = smemState[2 * kBQ + qi];
+    const float lr1 = smemState[3 * kBQ + qi];
     // a group state with l = 0 saw no key (m = -inf) and contributes nothing
     const float m = l1 > 0.f ? (l_tot > 0.f ? fmaxf(st.m, m1) : m1) : st.m;
     const float s0 = l_tot > 0.f ? __builtin_amdgcn_exp2f(st.m - m) : 0.f;
@@ -1337,6 +1633,7 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
     const float e1 = l1 > 0.f ? s1 * (a1 + l1 * (m1 - m)) : 0.f;
     a_tot = e0 + e1;
     l_tot = s0 * l_tot + s1 * l1;
+    lr_tot = s0 * lr_tot + s1 * lr1;
     const float4* src = (const float4*)(smem + GROUP_BYTES);
 #pragma unroll
     for (int j = 0; j < 4 * G::D_TILES; ++j) {
@@ -1352,7 +1649,7 @@ __device__ __forceinline__ void fused_row(int r, uint8_t* smem, float* smemState
 
   if (!qvalid) return;
   const size_t tok = (size_t)bh * N + qrow;
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float inv = lr_tot > 0.f ? 1.f / lr_tot : 0.f;
   uint16_t* dst = o + tok * D;
 #pragma unroll
   for (int dt = 0; dt < G::D_TILES; ++dt)
@@ -1378,7 +1675,7 @@ __global__ __launch_bounds__(kFusedThreads, 1) void attn_fused_kernel(
     int32_t* __restrict__ ctr) {
   constexpr int TILE = kBK * D * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILE];
-  __shared__ float smemState[3 * kBQ];
+  __shared__ float smemState[4 * kBQ];
   __shared__ int s_row, s_steal;
   if (threadIdx.x == 0) s_steal = 0;
   for (;;) {
@@ -1446,6 +1743,18 @@ hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
 }
 
 }  // namespace
+
+int k64_sparse_grid_cap(const tra_plan_s& p) {
+  return p.cfg.head_dim == 64 ? k64_sparse_grid_cap_d<64>(p) : k64_sparse_grid_cap_d<128>(p);
+}
+
+void split_capacities(int grid_cap, int rows, int head_dim, int* units_cap, int* splits_cap, int* slots_cap) {
+  const long long share = (long long)grid_cap * kSplitPerWG;
+  *units_cap = (int)std::min<long long>(INT_MAX, rows + share + 1);
+  *splits_cap = (int)std::min<long long>(INT_MAX, share + 1);
+  const long long slot_bytes = (long long)kBQ * (head_dim + 3) * 4;
+  *slots_cap = (int)std::min<long long>(2 * share + 1, kSplitSlotBytes / slot_bytes);
+}
 
 hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   if (p.cfg.head_dim == 64) return launch_bf16_d<64>(p, a, s);

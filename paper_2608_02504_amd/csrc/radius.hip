@@ -8,9 +8,11 @@
 //  n     = min{n in [0, n_cap] : C(n) >= K_hat}, else FULL        Eq. 14
 //
 // The paper tabulates the counts (App. C.1, a lookup table over query
-// coordinate and radius).  Here the counts are exact integer lattice counts
-// evaluated on the fly, row by row, so no per-shape count table has to live in
-// HBM; C(n) is non-decreasing in n, so the minimum is found by bisection.
+// coordinate and radius).  Here only the count at the largest candidate
+// radius is tabulated per position (it decides the full radius); other counts
+// are exact integer lattice counts evaluated on the fly, row by row, so no
+// per-shape table over every radius has to live in HBM.  C(n) is
+// non-decreasing in n, so the minimum is found by bisection.
 #include "tra_internal.h"
 
 namespace tra {
@@ -60,11 +62,22 @@ __device__ int grid_count(int f, int x, int y, int n, const int32_t* __restrict_
   return total;
 }
 
+// C(n_cap) of every video position (raster order), the count at the largest
+// candidate radius: a query whose budget exceeds it gets the full radius.  A
+// per-plan lookup table, filled once when the plan is created.
+__global__ __launch_bounds__(256) void cap_count_kernel(const int32_t* __restrict__ thr, int32_t* __restrict__ out,
+                                                        int N, int F, int H, int W, int n_cap) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int f = i / (H * W), x = (i / W) % H, y = i % W;
+  out[i] = grid_count(f, x, y, n_cap, thr, F, H, W);
+}
+
 template <int MAP>
 __global__ __launch_bounds__(256) void budget_radius_kernel(
     const float* __restrict__ entropy, int32_t* __restrict__ budget, int32_t* __restrict__ radius_sq,
-    const int32_t* __restrict__ thr, int total, int S, int N, int F, int H, int W, int n_cap,
-    double tau, double z_tau) {
+    const int32_t* __restrict__ thr, const int32_t* __restrict__ cap_count, int total, int S, int N, int F,
+    int H, int W, int n_cap, double tau, double z_tau) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
   const int i = idx % S;  // token: raster index for video, >= N for text
@@ -92,23 +105,32 @@ __global__ __launch_bounds__(256) void budget_radius_kernel(
 
   const int f = i / (H * W), x = (i / W) % H, y = i % W;
   int n;
+  const int c_cap = cap_count[i];
   if (khat <= F) {
     n = 0;  // C(0) = F: the query's own position in every frame
-  } else if (grid_count(f, x, y, n_cap, thr, F, H, W) < khat) {
+  } else if (c_cap < khat) {
     n = TRA_RADIUS_FULL;
   } else {
+    // Smallest n with C(n) >= khat by bisection: C(0) = F < khat, and
+    // C(n_cap) >= khat from the table.
     int lo = 0, hi = n_cap;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
+    while (hi - lo > 1) {
+      const int mid = lo + ((hi - lo) >> 1);
       if (grid_count(f, x, y, mid, thr, F, H, W) >= khat) hi = mid;
-      else lo = mid + 1;
+      else lo = mid;
     }
-    n = lo;
+    n = hi;
   }
   radius_sq[idx] = n;
 }
 
 }  // namespace
+
+hipError_t fill_cap_counts(const tra_plan_s& p, int32_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(cap_count_kernel, dim3((p.N + 255) / 256), dim3(256), 0, s, p.d_thr, out, p.N,
+                     p.cfg.frames, p.cfg.height, p.cfg.width, p.n_cap);
+  return hipGetLastError();
+}
 
 hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
                                 int32_t* radius_sq, hipStream_t s) {
@@ -117,11 +139,11 @@ hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32
   const dim3 grid((total + threads - 1) / threads);
   if (p.cfg.budget_map == TRA_BUDGET_LOGNORMAL)
     hipLaunchKernelGGL(budget_radius_kernel<TRA_BUDGET_LOGNORMAL>, grid, dim3(threads), 0, s, entropy,
-                       budget, radius_sq, p.d_thr, total, p.S, p.N, p.cfg.frames, p.cfg.height,
+                       budget, radius_sq, p.d_thr, p.d_cap_count, total, p.S, p.N, p.cfg.frames, p.cfg.height,
                        p.cfg.width, p.n_cap, p.cfg.tau, p.z_tau);
   else
     hipLaunchKernelGGL(budget_radius_kernel<TRA_BUDGET_UNIFORM>, grid, dim3(threads), 0, s, entropy,
-                       budget, radius_sq, p.d_thr, total, p.S, p.N, p.cfg.frames, p.cfg.height,
+                       budget, radius_sq, p.d_thr, p.d_cap_count, total, p.S, p.N, p.cfg.frames, p.cfg.height,
                        p.cfg.width, p.n_cap, p.cfg.tau, p.z_tau);
   return hipGetLastError();
 }

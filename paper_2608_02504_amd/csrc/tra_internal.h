@@ -61,6 +61,7 @@ struct tra_plan_s {
   int32_t* d_thr = nullptr;
   int32_t* d_thr1 = nullptr;  // 1-D thresholds (TRA_DIST_1D plans only)
   int32_t* d_blocks = nullptr;
+  int32_t* d_cap_count = nullptr;  // [N] C(n_cap) per video position (raster)
   int32_t* d_sort_ws = nullptr;  // counting-sort workspace of the row order
   int64_t sort_ws_elems = 0;
   int32_t sort_chunks = 0;
@@ -78,6 +79,17 @@ struct tra_plan_s {
   // (kRowCounters ints, reset by each call on its stream), and the CU count
   int32_t* d_row_ctr = nullptr;
   int32_t n_cu = 0;
+  // bf16 plans: work units of block-sparse calls (rows cut into pieces of at
+  // most L list entries) and the pieces' partial results: units [units_cap]
+  // int4, split rows [splits_cap] int4, header {units, split rows, L}, partial
+  // outputs [slots_cap][128][d] fp32 and statistics [slots_cap][3][128] fp32
+  // (running max, rounded and fp32 sums), for at most split_wg_cap workgroups.
+  int32_t split_wg_cap = 0, units_cap = 0, splits_cap = 0, slots_cap = 0;
+  int32_t* d_units = nullptr;
+  int32_t* d_splits = nullptr;
+  int32_t* d_unit_hdr = nullptr;
+  float* d_part = nullptr;
+  float* d_pstats = nullptr;
 };
 
 namespace tra {
@@ -100,10 +112,16 @@ struct AttnArgs {
   const int32_t* radius_sq = nullptr;  // token-level attention (sparse) only
 };
 hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
+// Largest grid of the block-sparse attention kernel on this plan's device, and
+// the work-unit table capacities for that grid.
+int k64_sparse_grid_cap(const tra_plan_s& p);
+void split_capacities(int grid_cap, int rows, int head_dim, int* units_cap, int* splits_cap, int* slots_cap);
 hipError_t launch_attention_f32(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
 
 hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
                                 int32_t* radius_sq, hipStream_t s);
+// Fills the plan's per-position table of C(n_cap) (once, at plan creation).
+hipError_t fill_cap_counts(const tra_plan_s& p, int32_t* out, hipStream_t s);
 
 hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask,
                              int32_t* cnt, int32_t* cols, hipStream_t s);
