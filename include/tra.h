@@ -212,6 +212,21 @@ tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t
                                 int32_t* cnt, int32_t* cols, int32_t* order,
                                 void* stream);
 
+/* tra_build_block_mask without any allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid it): the same mask, lists and order, bit for bit,
+ * but the heaviest-first order sorts in a scratch array that the library
+ * holds on each GPU (4 MiB, kept until the process ends) instead of the
+ * plan's workspace.  With a non-NULL order it needs (NB + 1) *
+ * ceil(batch * heads * NB / 256) <= 2^20 workspace ints and otherwise returns
+ * TRA_ERR_UNSUPPORTED before launching anything.  All calls on one GPU share
+ * that array: two such calls that overlap in time on that GPU (different
+ * streams) race; calls on one stream are ordered and safe.  Nothing here
+ * calls hipMalloc or hipFree. */
+tra_status tra_build_block_mask_noalloc(tra_plan plan, const int32_t* radius_sq, uint8_t* mask,
+                                        int32_t* cnt, int32_t* cols, int32_t* order,
+                                        void* stream);
+
 /* Block-sparse attention: a query of block u takes one softmax over every key
  * of the key blocks cols[r][0..cnt[r]) (r its row) and attends to no other key
  * (Eq. 16 at block granularity).  With a non-NULL `order`, only the rows it

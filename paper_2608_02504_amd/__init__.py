@@ -22,7 +22,7 @@ import numpy as np
 __all__ = [
     "LIB_PATH", "TRA_RADIUS_FULL", "TraError", "Config", "Plan", "lib", "library_loaded",
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
-    "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
+    "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
     "tra_sparse_attention", "tra_token_attention", "tra_dense_attention", "tra_version",
     "EXPORTED_SYMBOLS",
 ]
@@ -40,6 +40,7 @@ EXPORTED_SYMBOLS = (
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
     "tra_last_error", "tra_version", "tra_entropy", "tra_budget_radius",
     "tra_build_block_mask", "tra_sparse_attention", "tra_token_attention", "tra_dense_attention",
+    "tra_build_block_mask_noalloc",
 )
 
 _STATUS = {0: "TRA_OK", 1: "TRA_ERR_INVALID_ARG", 2: "TRA_ERR_UNSUPPORTED",
@@ -131,11 +132,12 @@ def lib() -> ctypes.CDLL:
     L.tra_entropy.argtypes = [P, V, V, V, V, V, V]
     L.tra_budget_radius.argtypes = [P, V, V, V, V]
     L.tra_build_block_mask.argtypes = [P, V, V, V, V, V, V]
+    L.tra_build_block_mask_noalloc.argtypes = [P, V, V, V, V, V, V]
     L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V]
     L.tra_token_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, V]
     L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V]
     for name in ("tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
-                 "tra_entropy", "tra_budget_radius", "tra_build_block_mask",
+                 "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
                  "tra_sparse_attention", "tra_token_attention", "tra_dense_attention"):
         getattr(L, name).restype = I
     _lib = L
@@ -285,6 +287,18 @@ def tra_build_block_mask(plan: Plan, radius_sq, mask, cnt, cols, order=None, str
     _want(order, (plan.rows,), torch.int32, "order")
     _check(lib().tra_build_block_mask(plan.handle, _ptr(radius_sq), _ptr(mask), _ptr(cnt),
                                       _ptr(cols), _ptr(order), _stream(stream)))
+
+
+def tra_build_block_mask_noalloc(plan: Plan, radius_sq, mask, cnt, cols, order=None, stream=None):
+    import torch
+    _, per, rowsh, sq = _shapes(plan)
+    _want(radius_sq, per, torch.int32, "radius_sq")
+    _want(mask, sq, torch.uint8, "mask")
+    _want(cnt, rowsh, torch.int32, "cnt")
+    _want(cols, sq, torch.int32, "cols")
+    _want(order, (plan.rows,), torch.int32, "order")
+    _check(lib().tra_build_block_mask_noalloc(plan.handle, _ptr(radius_sq), _ptr(mask), _ptr(cnt),
+                                              _ptr(cols), _ptr(order), _stream(stream)))
 
 
 def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, stream=None):

@@ -204,6 +204,13 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
         return fail(TRA_ERR_ALLOC, std::string("plan work-unit tables: ") + hipGetErrorString(e));
       }
     }
+    // the no-allocation entry point's scratch array on this device: its
+    // address is resolved here, once per device, with the device current
+    int32_t* scratch_ptr = nullptr;
+    if ((e = tra::resolve_noalloc_scratch(dev, &scratch_ptr)) != hipSuccess) {
+      tra_plan_destroy(p);
+      return hip_fail(e, "hipGetSymbolAddress of the no-allocation scratch");
+    }
     *out = p;
     return ok();
   } catch (const std::bad_alloc&) {
@@ -264,6 +271,28 @@ tra_status tra_build_block_mask(tra_plan p, const int32_t* radius_sq, uint8_t* m
   if (order) {
     e = tra::launch_row_order(*p, cnt, order, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask order launch");
+  }
+  return ok();
+}
+
+tra_status tra_build_block_mask_noalloc(tra_plan p, const int32_t* radius_sq, uint8_t* mask,
+                                        int32_t* cnt, int32_t* cols, int32_t* order, void* stream) {
+  TRA_TRY(check_plan(p));
+  TRA_TRY(check_aligned4(radius_sq, "radius_sq", false));
+  TRA_TRY(check_aligned4(cnt, "cnt", false));
+  TRA_TRY(check_aligned4(cols, "cols", false));
+  TRA_TRY(check_aligned4(order, "order", true));
+  const int64_t need = (int64_t)(p->NB + 1) * p->sort_chunks;
+  if (order && need > tra::kNoAllocScratchInts)
+    return fail(TRA_ERR_UNSUPPORTED,
+                "tra_build_block_mask_noalloc: the row order needs " + std::to_string(need) +
+                    " workspace ints, above the scratch array's " + std::to_string(tra::kNoAllocScratchInts) +
+                    " ((NB + 1) * ceil(batch * heads * NB / 256) must stay within it)");
+  hipError_t e = tra::launch_block_mask(*p, radius_sq, mask, cnt, cols, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask_noalloc launch");
+  if (order) {
+    e = tra::launch_row_order_noalloc(*p, cnt, order, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask_noalloc order launch");
   }
   return ok();
 }

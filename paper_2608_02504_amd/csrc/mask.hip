@@ -21,6 +21,7 @@
 // a block holding any text token is retained in every row, and the row of such
 // a block retains every key block.
 #include <climits>
+#include <mutex>
 
 #include "tra_internal.h"
 
@@ -420,19 +421,58 @@ hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint
   return hipGetLastError();
 }
 
-hipError_t launch_row_order(const tra_plan_s& p, const int32_t* cnt, int32_t* order, hipStream_t s) {
+hipError_t launch_row_order_ws(const tra_plan_s& p, const int32_t* cnt, int32_t* order, int32_t* ws,
+                               hipStream_t s) {
   const int chunks = p.sort_chunks;
-  hipLaunchKernelGGL(order_hist_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, p.d_sort_ws, p.rows,
-                     p.NB, chunks);
+  hipLaunchKernelGGL(order_hist_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, ws, p.rows, p.NB, chunks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, s, p.d_sort_ws,
-                     (int)((int64_t)(p.NB + 1) * chunks));
+  hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, s, ws, (int)((int64_t)(p.NB + 1) * chunks));
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(order_scatter_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, p.d_sort_ws, order,
-                     p.rows, p.NB, chunks);
+  hipLaunchKernelGGL(order_scatter_kernel, dim3(chunks), dim3(kSortChunk), 0, s, cnt, ws, order, p.rows, p.NB,
+                     chunks);
   return hipGetLastError();
+}
+
+hipError_t launch_row_order(const tra_plan_s& p, const int32_t* cnt, int32_t* order, hipStream_t s) {
+  return launch_row_order_ws(p, cnt, order, p.d_sort_ws, s);
+}
+
+// ------------------------------------------------ no-allocation entry point
+// The counting-sort workspace of tra_build_block_mask_noalloc: a device array
+// of the library itself, one copy per GPU, held until the process ends.  In
+// host code `scratch` only names the symbol; its device address on each GPU
+// comes from hipGetSymbolAddress (resolve_noalloc_scratch) and only that
+// address is handed to kernels.  Every order kernel writes each workspace
+// entry it later reads, so no clearing is needed between calls.
+static __device__ __align__(256) int32_t scratch[kNoAllocScratchInts];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t resolve_noalloc_scratch(int device, int32_t** out) {
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    int32_t* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = ptr;
+  }
+  *out = g_scratch_ptr[device];
+  return hipSuccess;
+}
+
+hipError_t launch_row_order_noalloc(const tra_plan_s& p, const int32_t* cnt, int32_t* order, hipStream_t s) {
+  int32_t* ws = nullptr;
+  const hipError_t e = resolve_noalloc_scratch(p.device, &ws);
+  if (e != hipSuccess) return e;
+  return launch_row_order_ws(p, cnt, order, ws, s);
 }
 
 }  // namespace tra

@@ -129,4 +129,13 @@ hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint
 hipError_t launch_row_order(const tra_plan_s& p, const int32_t* cnt, int32_t* order,
                             hipStream_t s);
 
+// The no-allocation variant: the same order with its counting-sort workspace
+// in the library's per-device scratch array of kNoAllocScratchInts ints.
+constexpr int64_t kNoAllocScratchInts = (int64_t)1 << 20;  // 4 MiB
+// Device address of that array on `device` (the current device), resolved once
+// per device and kept.
+hipError_t resolve_noalloc_scratch(int device, int32_t** out);
+hipError_t launch_row_order_noalloc(const tra_plan_s& p, const int32_t* cnt, int32_t* order,
+                                    hipStream_t s);
+
 }  // namespace tra
