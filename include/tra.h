@@ -51,25 +51,37 @@
  * ------------------------
  * Every compute call is asynchronous on `stream` (a hipStream_t passed as
  * void*, NULL = the null stream), checks its arguments before launching, and
- * returns a status.  The caller owns every tensor buffer and keeps it alive
- * until the stream has drained.  The plan owns its small device tables, a
- * sort workspace and, for bf16 plans, a key/value workspace of
- * 2 x batch x heads x NB x 128 x head_dim x 2 bytes into which every
- * attention call (tra_entropy, tra_sparse_attention, tra_token_attention,
- * tra_dense_attention)
- * first rewrites K and V in tile-major order (V transposed per block), and
- * 512 bytes of row-queue counters that the block-sparse and dense calls reset
- * and then draw their query-block rows from.  Calls
- * that share a plan must therefore not overlap in time on different streams
- * when they use a workspace (those calls on bf16 plans, and
- * tra_build_block_mask with a non-NULL order); calls on one stream are ordered
- * and safe.  Otherwise the plan is immutable after creation.  No C++
- * exception crosses this ABI.  On failure, tra_last_error() returns a message
- * for the calling thread.
+ * returns a status.  The caller owns every buffer -- tensors and workspaces
+ * -- and keeps it alive until the stream has drained.  The plan owns only its
+ * device tables (permutation, thresholds, block boxes, per-position counts at
+ * the largest radius, key-block distance words); no call writes them, so a
+ * plan is immutable after creation and may be shared by calls on any number
+ * of streams at once.
+ *
+ * Calls that need scratch device memory take it from the caller as
+ * (workspace, workspace_bytes): a device buffer, 256-byte aligned, of at least
+ * tra_workspace_size(plan, call) bytes.  Its contents need no initialisation
+ * and are undefined after the call.  Calls whose use of one workspace overlaps
+ * in time (different streams) race; give each stream its own.  What a bf16
+ * plan's workspace holds:
+ *   attention calls (tra_entropy, tra_sparse_attention, tra_token_attention,
+ *     tra_dense_attention): K and V rewritten in tile-major order (V
+ *     transposed in 64-key tiles), 2 x batch x heads x NB x 128 x head_dim x 2
+ *     bytes, rewritten by every call, plus 512 bytes of row-queue counters
+ *     that the call resets and draws its query-block rows from;
+ *   tra_sparse_attention, in addition: the work-unit tables and the split
+ *     rows' partial results (at most 256 MiB, see that call);
+ *   tra_build_block_mask with a non-NULL order: the counting-sort histograms
+ *     of the row order, 4 x ((NB + 1) x ceil(batch x heads x NB / 256) + 1)
+ *     bytes (the only workspace of fp32 plans; with a NULL order the mask call
+ *     needs none and the workspace may be NULL).
+ * No C++ exception crosses this ABI.  On failure, tra_last_error() returns a
+ * message for the calling thread.
  */
 #ifndef TRA_H
 #define TRA_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -132,6 +144,15 @@ typedef struct tra_config {
 
 typedef struct tra_plan_s* tra_plan;
 
+/* The calls that take a workspace, for tra_workspace_size. */
+typedef enum {
+  TRA_CALL_ENTROPY = 0,    /* tra_entropy (entropy only or fused with o)      */
+  TRA_CALL_BLOCK_MASK = 1, /* tra_build_block_mask with a non-NULL order      */
+  TRA_CALL_SPARSE = 2,     /* tra_sparse_attention                            */
+  TRA_CALL_TOKEN = 3,      /* tra_token_attention                             */
+  TRA_CALL_DENSE = 4       /* tra_dense_attention                             */
+} tra_call;
+
 /* Validates cfg, builds the shape tables on the host in fp64/integer
  * arithmetic (tile-major permutation, squared-radius thresholds
  * thr[n][delta] = floor(n * exp(-2 gamma delta)) for n in [0, n_cap],
@@ -161,6 +182,11 @@ tra_status tra_plan_dims(tra_plan plan, int32_t* n_tokens, int32_t* n_blocks,
 tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
                                 int32_t* thr1, int32_t* blocks, int32_t* n_cap_out);
 
+/* *bytes = the workspace size (bytes) that `call` (a tra_call) needs on this
+ * plan; 0 means the call takes none (its workspace may be NULL).  The size
+ * depends on the plan only, not on the call's data. */
+tra_status tra_workspace_size(tra_plan plan, int32_t call, size_t* bytes);
+
 /* Message describing the last failure on the calling thread ("" if none). */
 const char* tra_last_error(void);
 
@@ -177,9 +203,10 @@ const char* tra_version(void);
  * (the key blocks split over two groups of waves and merged), so its o and
  * entropy agree with tra_dense_attention's output and with the entropy-only
  * call up to fp32 rounding, not bit for bit; fp32 plans share one kernel.
- * entropy: fp32 [batch][heads][S] output. */
+ * entropy: fp32 [batch][heads][S] output.  workspace: TRA_CALL_ENTROPY. */
 tra_status tra_entropy(tra_plan plan, const void* q, const void* k, const void* v,
-                       void* o, float* entropy, void* stream);
+                       void* o, float* entropy, void* workspace, size_t workspace_bytes,
+                       void* stream);
 
 /* Entropy -> budget -> squared radius, per token (Sec. 3.1-3.2; App. C.1,
  * Eq. implementation-budget-radius).
@@ -206,18 +233,19 @@ tra_status tra_budget_radius(tra_plan plan, const float* entropy, int32_t* budge
  * distance come from the plan.  Text blocks are retained in every row and a
  * text block's row retains every block (Alg. 1; text keys stay visible). 
  * mask: uint8 output or NULL; cnt, cols: int32 outputs; order: int32 output
- * (the heaviest-first row order, sorted in the plan's sort workspace) or NULL
- * (not computed). */
+ * (the heaviest-first row order, sorted in the workspace) or NULL (not
+ * computed).  workspace: TRA_CALL_BLOCK_MASK when order is non-NULL, else
+ * unused (may be NULL). */
 tra_status tra_build_block_mask(tra_plan plan, const int32_t* radius_sq, uint8_t* mask,
                                 int32_t* cnt, int32_t* cols, int32_t* order,
-                                void* stream);
+                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* tra_build_block_mask without any allocation, for callers that cannot
  * allocate device memory (code under HIP graph capture, serving loops,
  * harnesses that forbid it): the same mask, lists and order, bit for bit,
  * but the heaviest-first order sorts in a scratch array that the library
- * holds on each GPU (4 MiB, kept until the process ends) instead of the
- * plan's workspace.  With a non-NULL order it needs (NB + 1) *
+ * holds on each GPU (4 MiB, kept until the process ends) instead of a
+ * caller's workspace.  With a non-NULL order it needs (NB + 1) *
  * ceil(batch * heads * NB / 256) <= 2^20 workspace ints and otherwise returns
  * TRA_ERR_UNSUPPORTED before launching anything.  All calls on one GPU share
  * that array: two such calls that overlap in time on that GPU (different
@@ -239,16 +267,19 @@ tra_status tra_build_block_mask_noalloc(tra_plan plan, const int32_t* radius_sq,
  * Work is balanced by cutting long lists: with T the total of the (clamped)
  * list lengths of the rows computed and G the number of workgroups the GPU
  * holds at once, a row of more than L = max(48, ceil(T / 16G)) entries (L
- * doubled while the pieces would not fit the plan's 256 MiB partial workspace)
+ * doubled while the pieces would not fit the 256 MiB of partial results the
+ * workspace holds)
  * is computed as ceil(cnt / L) pieces of consecutive entries whose partial
  * softmax states are merged afterwards, so its result differs from an
  * unsplit computation by rounding only (each piece rounds its probabilities
  * to bf16 relative to its own running maximum); rows of at most 48 entries
  * are never split.  The output is normalised by the sum of the
- * bf16-rounded probabilities that multiply V (lse by the fp32 sum). */
+ * bf16-rounded probabilities that multiply V (lse by the fp32 sum).
+ * workspace: TRA_CALL_SPARSE. */
 tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
                                 const void* v, const int32_t* cnt, const int32_t* cols,
-                                const int32_t* order, void* o, float* lse, void* stream);
+                                const int32_t* order, void* o, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /* Token-level TRA attention inside the retained blocks (Sec. 3.2, Eq. 16 with
  * the -inf bias of the token mask, Eq. 15; App. D names the block-granular
@@ -268,16 +299,19 @@ tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
  * of a wave's 32 queries covers are skipped.  bf16 plans need every threshold
  * below 65536 (n_cap <= 65535 for 2-D, floor(pi/2 n_cap) <= 65535 for 1-D)
  * and at least one block of video tokens per frame (H*W >= block), else
- * TRA_ERR_UNSUPPORTED. */
+ * TRA_ERR_UNSUPPORTED.  workspace: TRA_CALL_TOKEN. */
 tra_status tra_token_attention(tra_plan plan, const void* q, const void* k, const void* v,
                                const int32_t* radius_sq, const int32_t* cnt,
                                const int32_t* cols, const int32_t* order, void* o,
-                               float* lse, void* stream);
+                               float* lse, void* workspace, size_t workspace_bytes,
+                               void* stream);
 
 /* Dense attention o_i = sum_j softmax_j(q_i k_j / sqrt(d)) v_j (Eq. 1), the
- * baseline the sparse call is measured against.  lse as above, or NULL. */
+ * baseline the sparse call is measured against.  lse as above, or NULL.
+ * workspace: TRA_CALL_DENSE. */
 tra_status tra_dense_attention(tra_plan plan, const void* q, const void* k,
-                               const void* v, void* o, float* lse, void* stream);
+                               const void* v, void* o, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

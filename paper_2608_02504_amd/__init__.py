@@ -5,8 +5,13 @@ marshals arguments: every step of the path runs in the library's HIP kernels.
 torch is used for device memory and streams.  The functions keep the C names:
 
     tra_plan_create / tra_plan_destroy / tra_plan_dims / tra_plan_host_tables
-    tra_entropy / tra_budget_radius / tra_build_block_mask
+    tra_workspace_size / tra_entropy / tra_budget_radius / tra_build_block_mask
     tra_sparse_attention / tra_token_attention / tra_dense_attention
+
+Calls that take a workspace accept one as `workspace=` (a uint8 CUDA tensor of
+at least tra_workspace_size bytes); without one, the Plan keeps a workspace per
+stream, allocated through torch on its first use on that stream, so calls on
+one stream reuse it and calls on different streams never share one.
 
 There is no fallback: if libtra.so is missing or fails to load, every call
 raises.
@@ -22,7 +27,8 @@ import numpy as np
 __all__ = [
     "LIB_PATH", "TRA_RADIUS_FULL", "TraError", "Config", "Plan", "lib", "library_loaded",
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
-    "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
+    "tra_workspace_size", "TRA_CALL_ENTROPY", "TRA_CALL_BLOCK_MASK", "TRA_CALL_SPARSE",
+    "TRA_CALL_TOKEN", "TRA_CALL_DENSE", "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
     "tra_sparse_attention", "tra_token_attention", "tra_dense_attention", "tra_version",
     "EXPORTED_SYMBOLS",
 ]
@@ -33,6 +39,8 @@ TRA_BF16, TRA_FP32 = 0, 1
 TRA_MASK_VOTE, TRA_MASK_UNION = 0, 1
 TRA_BUDGET_UNIFORM, TRA_BUDGET_LOGNORMAL = 0, 1
 TRA_DIST_2D, TRA_DIST_1D = 0, 1
+TRA_CALL_ENTROPY, TRA_CALL_BLOCK_MASK, TRA_CALL_SPARSE, TRA_CALL_TOKEN, TRA_CALL_DENSE = range(5)
+_CALLS = (TRA_CALL_ENTROPY, TRA_CALL_BLOCK_MASK, TRA_CALL_SPARSE, TRA_CALL_TOKEN, TRA_CALL_DENSE)
 _BUDGET = {"uniform": TRA_BUDGET_UNIFORM, "lognormal": TRA_BUDGET_LOGNORMAL}
 _DIST = {"2d": TRA_DIST_2D, "1d": TRA_DIST_1D}
 
@@ -40,7 +48,7 @@ EXPORTED_SYMBOLS = (
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
     "tra_last_error", "tra_version", "tra_entropy", "tra_budget_radius",
     "tra_build_block_mask", "tra_sparse_attention", "tra_token_attention", "tra_dense_attention",
-    "tra_build_block_mask_noalloc",
+    "tra_build_block_mask_noalloc", "tra_workspace_size",
 )
 
 _STATUS = {0: "TRA_OK", 1: "TRA_ERR_INVALID_ARG", 2: "TRA_ERR_UNSUPPORTED",
@@ -121,7 +129,7 @@ def lib() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run python -m paper_2608_02504_amd.build")
     L = ctypes.CDLL(LIB_PATH)
-    P, I, V = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
+    P, I, V, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
     cfgp = ctypes.POINTER(_Config)
     L.tra_plan_create.argtypes = [cfgp, ctypes.POINTER(P)]
     L.tra_plan_destroy.argtypes = [P]
@@ -129,14 +137,16 @@ def lib() -> ctypes.CDLL:
     L.tra_plan_host_tables.argtypes = [cfgp, P, P, P, P, P]
     L.tra_last_error.restype = ctypes.c_char_p
     L.tra_version.restype = ctypes.c_char_p
-    L.tra_entropy.argtypes = [P, V, V, V, V, V, V]
+    L.tra_workspace_size.argtypes = [P, ctypes.c_int32, ctypes.POINTER(Z)]
+    L.tra_entropy.argtypes = [P, V, V, V, V, V, V, Z, V]
     L.tra_budget_radius.argtypes = [P, V, V, V, V]
-    L.tra_build_block_mask.argtypes = [P, V, V, V, V, V, V]
+    L.tra_build_block_mask.argtypes = [P, V, V, V, V, V, V, Z, V]
     L.tra_build_block_mask_noalloc.argtypes = [P, V, V, V, V, V, V]
-    L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V]
-    L.tra_token_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, V]
-    L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V]
+    L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, Z, V]
+    L.tra_token_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, V, Z, V]
+    L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V, Z, V]
     for name in ("tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
+                 "tra_workspace_size",
                  "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
                  "tra_sparse_attention", "tra_token_attention", "tra_dense_attention"):
         getattr(L, name).restype = I
@@ -170,12 +180,15 @@ class Plan:
         n, nb, cap = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         _check(lib().tra_plan_dims(h, ctypes.byref(n), ctypes.byref(nb), ctypes.byref(cap)))
         self.n_tokens, self.n_blocks, self.n_cap = n.value, nb.value, cap.value
+        self._ws = {}  # stream handle -> workspace tensor of ws_bytes
+        self.ws_bytes = max(tra_workspace_size(self, c) for c in _CALLS)
 
     @property
     def rows(self) -> int:
         return self.cfg.batch * self.cfg.heads * self.n_blocks
 
     def close(self):
+        self._ws = {}
         if getattr(self, "handle", None) is not None and self.handle.value:
             lib().tra_plan_destroy(self.handle)
             self.handle = ctypes.c_void_p()
@@ -199,6 +212,13 @@ def tra_plan_create(cfg: Config) -> Plan:
 
 def tra_plan_destroy(plan: Plan):
     plan.close()
+
+
+def tra_workspace_size(plan: Plan, call: int) -> int:
+    """Bytes of workspace `call` (a TRA_CALL_* value) needs on this plan."""
+    n = ctypes.c_size_t()
+    _check(lib().tra_workspace_size(plan.handle, call, ctypes.byref(n)))
+    return n.value
 
 
 def tra_plan_dims(plan: Plan):
@@ -238,6 +258,27 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
+def _workspace(plan: Plan, stream, workspace):
+    """(pointer, bytes, tensor) of the workspace for a call on `stream`: the
+    caller's, or the plan's own for that stream (created on first use)."""
+    import torch
+    if workspace is not None:
+        if workspace.dtype != torch.uint8:
+            raise ValueError("workspace must be a uint8 tensor")
+        return _ptr(workspace), workspace.numel(), workspace
+    if plan.ws_bytes == 0:
+        return None, 0, None
+    handle = _stream(stream).value or 0
+    ws = plan._ws.get(handle)
+    if ws is None:
+        ws = torch.empty(plan.ws_bytes, dtype=torch.uint8, device="cuda")
+        if handle != (torch.cuda.current_stream().cuda_stream or 0):
+            # freed only when the plan closes: keep it until that stream's work is done
+            ws.record_stream(torch.cuda.ExternalStream(handle))
+        plan._ws[handle] = ws
+    return ctypes.c_void_p(ws.data_ptr()), ws.numel(), ws
+
+
 def _want(t, shape, dtype, name):
     if t is None:
         return
@@ -256,15 +297,16 @@ def _shapes(plan: Plan):
             (c.batch, c.heads, plan.n_blocks), (c.batch, c.heads, plan.n_blocks, plan.n_blocks))
 
 
-def tra_entropy(plan: Plan, q, k, v, o, entropy, stream=None):
+def tra_entropy(plan: Plan, q, k, v, o, entropy, stream=None, workspace=None):
     import torch
     tok, per, _, _ = _shapes(plan)
     dt = _qkv_dtype(plan)
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
         _want(t, tok, dt, n)
     _want(entropy, per, torch.float32, "entropy")
+    wp, wn, _ = _workspace(plan, stream, workspace)
     _check(lib().tra_entropy(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(entropy),
-                             _stream(stream)))
+                             wp, wn, _stream(stream)))
 
 
 def tra_budget_radius(plan: Plan, entropy, budget, radius_sq, stream=None):
@@ -277,7 +319,7 @@ def tra_budget_radius(plan: Plan, entropy, budget, radius_sq, stream=None):
                                    _stream(stream)))
 
 
-def tra_build_block_mask(plan: Plan, radius_sq, mask, cnt, cols, order=None, stream=None):
+def tra_build_block_mask(plan: Plan, radius_sq, mask, cnt, cols, order=None, stream=None, workspace=None):
     import torch
     _, per, rowsh, sq = _shapes(plan)
     _want(radius_sq, per, torch.int32, "radius_sq")
@@ -285,8 +327,9 @@ def tra_build_block_mask(plan: Plan, radius_sq, mask, cnt, cols, order=None, str
     _want(cnt, rowsh, torch.int32, "cnt")
     _want(cols, sq, torch.int32, "cols")
     _want(order, (plan.rows,), torch.int32, "order")
+    wp, wn, _ = _workspace(plan, stream, workspace) if order is not None else (None, 0, None)
     _check(lib().tra_build_block_mask(plan.handle, _ptr(radius_sq), _ptr(mask), _ptr(cnt),
-                                      _ptr(cols), _ptr(order), _stream(stream)))
+                                      _ptr(cols), _ptr(order), wp, wn, _stream(stream)))
 
 
 def tra_build_block_mask_noalloc(plan: Plan, radius_sq, mask, cnt, cols, order=None, stream=None):
@@ -301,7 +344,7 @@ def tra_build_block_mask_noalloc(plan: Plan, radius_sq, mask, cnt, cols, order=N
                                               _ptr(cols), _ptr(order), _stream(stream)))
 
 
-def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, stream=None):
+def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, stream=None, workspace=None):
     import torch
     tok, per, rowsh, sq = _shapes(plan)
     dt = _qkv_dtype(plan)
@@ -311,12 +354,14 @@ def tra_sparse_attention(plan: Plan, q, k, v, cnt, cols, order, o, lse=None, str
     _want(cols, sq, torch.int32, "cols")
     _want(order, (plan.rows,), torch.int32, "order")
     _want(lse, per, torch.float32, "lse")
+    wp, wn, _ = _workspace(plan, stream, workspace)
     _check(lib().tra_sparse_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(cnt),
-                                      _ptr(cols), _ptr(order), _ptr(o), _ptr(lse),
+                                      _ptr(cols), _ptr(order), _ptr(o), _ptr(lse), wp, wn,
                                       _stream(stream)))
 
 
-def tra_token_attention(plan: Plan, q, k, v, radius_sq, cnt, cols, order, o, lse=None, stream=None):
+def tra_token_attention(plan: Plan, q, k, v, radius_sq, cnt, cols, order, o, lse=None, stream=None,
+                        workspace=None):
     import torch
     tok, per, rowsh, sq = _shapes(plan)
     dt = _qkv_dtype(plan)
@@ -327,17 +372,19 @@ def tra_token_attention(plan: Plan, q, k, v, radius_sq, cnt, cols, order, o, lse
     _want(cols, sq, torch.int32, "cols")
     _want(order, (plan.rows,), torch.int32, "order")
     _want(lse, per, torch.float32, "lse")
+    wp, wn, _ = _workspace(plan, stream, workspace)
     _check(lib().tra_token_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(radius_sq),
-                                     _ptr(cnt), _ptr(cols), _ptr(order), _ptr(o), _ptr(lse),
+                                     _ptr(cnt), _ptr(cols), _ptr(order), _ptr(o), _ptr(lse), wp, wn,
                                      _stream(stream)))
 
 
-def tra_dense_attention(plan: Plan, q, k, v, o, lse=None, stream=None):
+def tra_dense_attention(plan: Plan, q, k, v, o, lse=None, stream=None, workspace=None):
     import torch
     tok, per, _, _ = _shapes(plan)
     dt = _qkv_dtype(plan)
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
         _want(t, tok, dt, n)
     _want(lse, per, torch.float32, "lse")
+    wp, wn, _ = _workspace(plan, stream, workspace)
     _check(lib().tra_dense_attention(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
-                                     _stream(stream)))
+                                     wp, wn, _stream(stream)))

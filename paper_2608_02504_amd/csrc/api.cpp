@@ -68,6 +68,77 @@ tra_status launch_result(hipError_t e, const char* what) {
   return ok();
 }
 
+// ----------------------------------------------------------- call workspace
+// Device memory a call writes besides its outputs, carved from the caller's
+// workspace buffer (each piece 256-byte aligned).  The plan itself holds only
+// tables that no call writes.
+constexpr size_t kWsAlign = 256;
+
+struct WsLayout {
+  size_t kt = 0, vt = 0, ctr = 0, units = 0, splits = 0, hdr = 0, part = 0, pstats = 0, sort = 0;
+  size_t total = 0;
+};
+
+WsLayout ws_layout(const tra_plan_s& p, int call) {
+  WsLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + kWsAlign - 1) / kWsAlign * kWsAlign;
+    return at;
+  };
+  if (call == TRA_CALL_BLOCK_MASK) {
+    L.sort = take((size_t)p.sort_ws_elems * sizeof(int32_t));
+  } else if (p.cfg.dtype == TRA_BF16) {
+    const size_t kv = (size_t)p.cfg.batch * p.cfg.heads * p.n_pad * p.cfg.head_dim * sizeof(uint16_t);
+    L.kt = take(kv);
+    L.vt = take(kv);
+    L.ctr = take(tra::kRowCounters * sizeof(int32_t));
+    if (call == TRA_CALL_SPARSE) {
+      L.units = take((size_t)p.units_cap * 4 * sizeof(int32_t));
+      L.splits = take((size_t)p.splits_cap * 4 * sizeof(int32_t));
+      L.hdr = take(4 * sizeof(int32_t));
+      L.part = take((size_t)p.slots_cap * 128 * p.cfg.head_dim * sizeof(float));
+      L.pstats = take((size_t)p.slots_cap * 3 * 128 * sizeof(float));
+    }
+  }
+  L.total = off;
+  return L;
+}
+
+// Checks the caller's workspace for `call` and returns, in *out, a copy of the
+// plan whose per-call pointers address it.  `needed` is false where the call
+// writes no workspace (then the buffer may be NULL).
+tra_status bind_workspace(tra_plan p, int call, bool needed, void* ws, size_t ws_bytes, tra_plan_s* out) {
+  *out = *p;
+  const WsLayout L = ws_layout(*p, call);
+  if (!needed || L.total == 0) return TRA_OK;
+  if (!ws)
+    return fail(TRA_ERR_INVALID_ARG, "workspace is NULL; this call needs " + std::to_string(L.total) +
+                                         " bytes (tra_workspace_size)");
+  if (((uintptr_t)ws & (kWsAlign - 1)) != 0)
+    return fail(TRA_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+  if (ws_bytes < L.total)
+    return fail(TRA_ERR_INVALID_ARG, "workspace holds " + std::to_string(ws_bytes) + " bytes; this call needs " +
+                                         std::to_string(L.total) + " (tra_workspace_size)");
+  uint8_t* b = (uint8_t*)ws;
+  if (call == TRA_CALL_BLOCK_MASK) {
+    out->d_sort_ws = (int32_t*)(b + L.sort);
+    return TRA_OK;
+  }
+  out->d_kt = (uint16_t*)(b + L.kt);
+  out->d_vt = (uint16_t*)(b + L.vt);
+  out->d_row_ctr = (int32_t*)(b + L.ctr);
+  if (call == TRA_CALL_SPARSE) {
+    out->d_units = (int32_t*)(b + L.units);
+    out->d_splits = (int32_t*)(b + L.splits);
+    out->d_unit_hdr = (int32_t*)(b + L.hdr);
+    out->d_part = (float*)(b + L.part);
+    out->d_pstats = (float*)(b + L.pstats);
+  }
+  return TRA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -109,16 +180,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_thr1);
   (void)hipFree(p->d_blocks);
   (void)hipFree(p->d_cap_count);
-  (void)hipFree(p->d_sort_ws);
-  (void)hipFree(p->d_kt);
-  (void)hipFree(p->d_vt);
   (void)hipFree(p->d_kinfo);
-  (void)hipFree(p->d_row_ctr);
-  (void)hipFree(p->d_units);
-  (void)hipFree(p->d_splits);
-  (void)hipFree(p->d_unit_hdr);
-  (void)hipFree(p->d_part);
-  (void)hipFree(p->d_pstats);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -171,8 +233,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
         (e = upload(&p->d_coord, t.coord)) != hipSuccess ||
         (e = upload(&p->d_thr, t.thr)) != hipSuccess ||
         (e = upload(&p->d_blocks, t.blocks)) != hipSuccess ||
-        (one_d && (e = upload(&p->d_thr1, t.thr1)) != hipSuccess) ||
-        (e = hipMalloc((void**)&p->d_sort_ws, p->sort_ws_elems * sizeof(int32_t))) != hipSuccess) {
+        (one_d && (e = upload(&p->d_thr1, t.thr1)) != hipSuccess)) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
     }
@@ -183,26 +244,13 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       return fail(TRA_ERR_ALLOC, std::string("plan count table: ") + hipGetErrorString(e));
     }
     if (cfg->dtype == TRA_BF16) {
-      const size_t bytes = (size_t)cfg->batch * cfg->heads * p->n_pad * cfg->head_dim * sizeof(uint16_t);
-      if ((e = hipMalloc((void**)&p->d_kt, bytes)) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_vt, bytes)) != hipSuccess ||
-          (e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_row_ctr, tra::kRowCounters * sizeof(int32_t))) != hipSuccess) {
+      if ((e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess) {
         tra_plan_destroy(p);
-        return fail(TRA_ERR_ALLOC, std::string("plan K/V workspace: ") + hipGetErrorString(e));
+        return fail(TRA_ERR_ALLOC, std::string("plan key-info table: ") + hipGetErrorString(e));
       }
       p->split_wg_cap = tra::k64_sparse_grid_cap(*p);
       tra::split_capacities(p->split_wg_cap, p->rows, cfg->head_dim, &p->units_cap, &p->splits_cap,
                            &p->slots_cap);
-      const size_t slot_floats = (size_t)128 * cfg->head_dim;
-      if ((e = hipMalloc((void**)&p->d_units, (size_t)p->units_cap * 4 * sizeof(int32_t))) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_splits, (size_t)p->splits_cap * 4 * sizeof(int32_t))) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_unit_hdr, 4 * sizeof(int32_t))) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_part, (size_t)p->slots_cap * slot_floats * sizeof(float))) != hipSuccess ||
-          (e = hipMalloc((void**)&p->d_pstats, (size_t)p->slots_cap * 3 * 128 * sizeof(float))) != hipSuccess) {
-        tra_plan_destroy(p);
-        return fail(TRA_ERR_ALLOC, std::string("plan work-unit tables: ") + hipGetErrorString(e));
-      }
     }
     // the no-allocation entry point's scratch array on this device: its
     // address is resolved here, once per device, with the device current
@@ -220,6 +268,15 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
   }
 }
 
+tra_status tra_workspace_size(tra_plan p, int32_t call, size_t* bytes) {
+  if (!p) return fail(TRA_ERR_INVALID_ARG, "plan is NULL");
+  if (!bytes) return fail(TRA_ERR_INVALID_ARG, "bytes is NULL");
+  if (call < TRA_CALL_ENTROPY || call > TRA_CALL_DENSE)
+    return fail(TRA_ERR_INVALID_ARG, "unknown call " + std::to_string(call));
+  *bytes = ws_layout(*p, call).total;
+  return ok();
+}
+
 tra_status tra_plan_dims(tra_plan p, int32_t* n_tokens, int32_t* n_blocks, int32_t* n_cap) {
   if (!p) return fail(TRA_ERR_INVALID_ARG, "plan is NULL");
   if (n_tokens) *n_tokens = p->S;
@@ -228,15 +285,18 @@ tra_status tra_plan_dims(tra_plan p, int32_t* n_tokens, int32_t* n_blocks, int32
   return ok();
 }
 
-static tra_status run_attention(tra_plan p, const tra::AttnArgs& a, void* stream, const char* what) {
+static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a, void* ws, size_t ws_bytes,
+                                void* stream, const char* what) {
+  tra_plan_s bound;
+  TRA_TRY(bind_workspace(p, call, true, ws, ws_bytes, &bound));
   hipError_t e = p->cfg.dtype == TRA_BF16
-                     ? tra::launch_attention_bf16(*p, a, (hipStream_t)stream)
-                     : tra::launch_attention_f32(*p, a, (hipStream_t)stream);
+                     ? tra::launch_attention_bf16(bound, a, (hipStream_t)stream)
+                     : tra::launch_attention_f32(bound, a, (hipStream_t)stream);
   return launch_result(e, what);
 }
 
 tra_status tra_entropy(tra_plan p, const void* q, const void* k, const void* v, void* o,
-                       float* entropy, void* stream) {
+                       float* entropy, void* workspace, size_t workspace_bytes, void* stream) {
   TRA_TRY(check_plan(p));
   TRA_TRY(check_tensor(q, "q"));
   TRA_TRY(check_tensor(k, "k"));
@@ -246,7 +306,7 @@ tra_status tra_entropy(tra_plan p, const void* q, const void* k, const void* v, 
   if ((v == nullptr) != (o == nullptr))
     return fail(TRA_ERR_INVALID_ARG, "v and o must be both NULL or both non-NULL");
   tra::AttnArgs a{q, k, v, o, nullptr, entropy, nullptr, nullptr, nullptr, false};
-  return run_attention(p, a, stream, "tra_entropy launch");
+  return run_attention(p, TRA_CALL_ENTROPY, a, workspace, workspace_bytes, stream, "tra_entropy launch");
 }
 
 tra_status tra_budget_radius(tra_plan p, const float* entropy, int32_t* budget,
@@ -260,16 +320,19 @@ tra_status tra_budget_radius(tra_plan p, const float* entropy, int32_t* budget,
 }
 
 tra_status tra_build_block_mask(tra_plan p, const int32_t* radius_sq, uint8_t* mask,
-                                int32_t* cnt, int32_t* cols, int32_t* order, void* stream) {
+                                int32_t* cnt, int32_t* cols, int32_t* order, void* workspace,
+                                size_t workspace_bytes, void* stream) {
   TRA_TRY(check_plan(p));
   TRA_TRY(check_aligned4(radius_sq, "radius_sq", false));
   TRA_TRY(check_aligned4(cnt, "cnt", false));
   TRA_TRY(check_aligned4(cols, "cols", false));
   TRA_TRY(check_aligned4(order, "order", true));
+  tra_plan_s bound;
+  TRA_TRY(bind_workspace(p, TRA_CALL_BLOCK_MASK, order != nullptr, workspace, workspace_bytes, &bound));
   hipError_t e = tra::launch_block_mask(*p, radius_sq, mask, cnt, cols, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask launch");
   if (order) {
-    e = tra::launch_row_order(*p, cnt, order, (hipStream_t)stream);
+    e = tra::launch_row_order(bound, cnt, order, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "tra_build_block_mask order launch");
   }
   return ok();
@@ -299,7 +362,8 @@ tra_status tra_build_block_mask_noalloc(tra_plan p, const int32_t* radius_sq, ui
 
 tra_status tra_sparse_attention(tra_plan p, const void* q, const void* k, const void* v,
                                 const int32_t* cnt, const int32_t* cols, const int32_t* order,
-                                void* o, float* lse, void* stream) {
+                                void* o, float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
   TRA_TRY(check_plan(p));
   TRA_TRY(check_tensor(q, "q"));
   TRA_TRY(check_tensor(k, "k"));
@@ -310,12 +374,13 @@ tra_status tra_sparse_attention(tra_plan p, const void* q, const void* k, const 
   TRA_TRY(check_aligned4(order, "order", true));
   TRA_TRY(check_aligned4(lse, "lse", true));
   tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true};
-  return run_attention(p, a, stream, "tra_sparse_attention launch");
+  return run_attention(p, TRA_CALL_SPARSE, a, workspace, workspace_bytes, stream, "tra_sparse_attention launch");
 }
 
 tra_status tra_token_attention(tra_plan p, const void* q, const void* k, const void* v,
                                const int32_t* radius_sq, const int32_t* cnt, const int32_t* cols,
-                               const int32_t* order, void* o, float* lse, void* stream) {
+                               const int32_t* order, void* o, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   TRA_TRY(check_plan(p));
   TRA_TRY(check_tensor(q, "q"));
   TRA_TRY(check_tensor(k, "k"));
@@ -333,11 +398,12 @@ tra_status tra_token_attention(tra_plan p, const void* q, const void* k, const v
       return fail(TRA_ERR_UNSUPPORTED, "token attention on bf16 plans needs height * width >= block");
   }
   tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true, radius_sq};
-  return run_attention(p, a, stream, "tra_token_attention launch");
+  return run_attention(p, TRA_CALL_TOKEN, a, workspace, workspace_bytes, stream, "tra_token_attention launch");
 }
 
 tra_status tra_dense_attention(tra_plan p, const void* q, const void* k, const void* v,
-                               void* o, float* lse, void* stream) {
+                               void* o, float* lse, void* workspace, size_t workspace_bytes,
+                               void* stream) {
   TRA_TRY(check_plan(p));
   TRA_TRY(check_tensor(q, "q"));
   TRA_TRY(check_tensor(k, "k"));
@@ -345,7 +411,7 @@ tra_status tra_dense_attention(tra_plan p, const void* q, const void* k, const v
   TRA_TRY(check_tensor(o, "o"));
   TRA_TRY(check_aligned4(lse, "lse", true));
   tra::AttnArgs a{q, k, v, o, lse, nullptr, nullptr, nullptr, nullptr, false};
-  return run_attention(p, a, stream, "tra_dense_attention launch");
+  return run_attention(p, TRA_CALL_DENSE, a, workspace, workspace_bytes, stream, "tra_dense_attention launch");
 }
 
 }  // extern "C"

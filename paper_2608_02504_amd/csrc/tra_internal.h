@@ -62,11 +62,15 @@ struct tra_plan_s {
   int32_t* d_thr1 = nullptr;  // 1-D thresholds (TRA_DIST_1D plans only)
   int32_t* d_blocks = nullptr;
   int32_t* d_cap_count = nullptr;  // [N] C(n_cap) per video position (raster)
-  int32_t* d_sort_ws = nullptr;  // counting-sort workspace of the row order
+  // Per-call device memory.  The pointers below marked "call workspace" are
+  // NULL in a stored plan, which no call writes; each call works on a copy of
+  // the plan with them pointing into the caller's workspace buffer.
+  int32_t* d_sort_ws = nullptr;  // call workspace: counting-sort histograms of the row order
   int64_t sort_ws_elems = 0;
   int32_t sort_chunks = 0;
-  // bf16 plans: K and V gathered into tile-major order, [batch*heads][NB*block][d],
-  // rows past S zero-filled, so the attention loop addresses tiles affinely.
+  // bf16 plans, call workspace: K and V gathered into tile-major order,
+  // [batch*heads][NB*block][d] (V transposed in 64-key tiles), rows past S
+  // zero-filled, so the attention loop addresses tiles affinely.
   int32_t n_pad = 0;
   uint16_t* d_kt = nullptr;
   uint16_t* d_vt = nullptr;
@@ -75,15 +79,16 @@ struct tra_plan_s {
   // the key side of the token mask inside a tile.
   int32_t* d_kinfo = nullptr;
   int32_t thr_max = 0;  // largest entry of the plan's threshold table
-  // bf16 plans: row-queue counters of the persistent attention kernel
-  // (kRowCounters ints, reset by each call on its stream), and the CU count
+  // bf16 plans, call workspace: row-queue counters of the persistent attention
+  // kernel (kRowCounters ints, reset by each call on its stream); the CU count
   int32_t* d_row_ctr = nullptr;
   int32_t n_cu = 0;
-  // bf16 plans: work units of block-sparse calls (rows cut into pieces of at
+  // bf16 plans, call workspace: work units of block-sparse calls (rows cut into pieces of at
   // most L list entries) and the pieces' partial results: units [units_cap]
   // int4, split rows [splits_cap] int4, header {units, split rows, L}, partial
   // outputs [slots_cap][128][d] fp32 and statistics [slots_cap][3][128] fp32
-  // (running max, rounded and fp32 sums), for at most split_wg_cap workgroups.
+  // (running max, rounded and fp32 sums), for at most split_wg_cap workgroups;
+  // the capacities are the plan's, fixed at creation.
   int32_t split_wg_cap = 0, units_cap = 0, splits_cap = 0, slots_cap = 0;
   int32_t* d_units = nullptr;
   int32_t* d_splits = nullptr;

@@ -93,11 +93,15 @@ def test_null_arguments_are_errors_not_crashes():
     L = tra.lib()
     assert L.tra_plan_host_tables(None, None, None, None, None, None) == 1
     assert L.tra_plan_create(None, None) == 1
-    assert L.tra_entropy(None, None, None, None, None, None, None) == 1
+    assert L.tra_workspace_size(None, 0, None) == 1
+    assert L.tra_entropy(None, None, None, None, None, None, None, 0, None) == 1
     assert L.tra_budget_radius(None, None, None, None, None) == 1
-    assert L.tra_build_block_mask(None, None, None, None, None, None, None) == 1
-    assert L.tra_sparse_attention(None, None, None, None, None, None, None, None, None, None) == 1
-    assert L.tra_dense_attention(None, None, None, None, None, None, None) == 1
+    assert L.tra_build_block_mask(None, None, None, None, None, None, None, 0, None) == 1
+    assert L.tra_build_block_mask_noalloc(None, None, None, None, None, None, None) == 1
+    assert L.tra_sparse_attention(None, None, None, None, None, None, None, None, None, None, 0, None) == 1
+    assert L.tra_token_attention(None, None, None, None, None, None, None, None, None, None, None, 0,
+                                 None) == 1
+    assert L.tra_dense_attention(None, None, None, None, None, None, None, 0, None) == 1
     assert b"NULL" in L.tra_last_error()
     assert L.tra_plan_destroy(None) == 0
     assert L.tra_last_error() == b""
