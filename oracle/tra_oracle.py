@@ -31,9 +31,11 @@ import torch
 from scipy.special import erfc
 
 RADIUS_FULL = 2 ** 31 - 1
+PAD = -1  # an empty position of a padded block layout
 
 __all__ = [
-    "RADIUS_FULL", "grid_coords", "tile_major_order", "block_bounds",
+    "RADIUS_FULL", "PAD", "grid_coords", "tile_major_order", "tile_aligned_order",
+    "block_tokens", "block_sizes", "block_bounds",
     "scores", "softmax_rows", "dense_attention", "entropy_from_probs",
     "entropy_from_scores", "token_budget", "n_cap", "threshold_table",
     "within_radius", "grid_count_bruteforce", "disk_count_table", "grid_count",
@@ -77,6 +79,50 @@ def joint_order(perm_video, text_tokens: int) -> np.ndarray:
     perm_video = np.asarray(perm_video, dtype=np.int64)
     n = perm_video.shape[0]
     return np.concatenate([perm_video, np.arange(n, n + text_tokens, dtype=np.int64)])
+
+
+def tile_aligned_order(F: int, H: int, W: int, tile_h: int, tile_w: int, b: int,
+                       text_tokens: int = 0) -> np.ndarray:
+    """Tile-aligned padded blocks: the tile-major order of Sec. 3.3 with every
+    block holding exactly one tile_h x tile_w tile of one frame (tile_h *
+    tile_w = b).  App. D names the work a retained block does on keys outside
+    a query's radius as the method's main limitation; a block that is one
+    spatial tile has the smallest footprint a block of b tokens can have.
+
+    Frames in order, tiles in tile-row-major order inside a frame, tokens
+    row-major inside a tile; a tile clipped by the frame edge fills the first
+    positions of its block and the rest of the block is padding (PAD).  Text
+    tokens N .. N+T-1 follow in blocks of b, the last one padded.  Returns perm
+    of length NB * b: perm[p] = token index at position p, or PAD.
+    """
+    if tile_h * tile_w != b:
+        raise ValueError("a tile must hold exactly one block")
+    out = []
+    for f in range(F):
+        for x0 in range(0, H, tile_h):
+            for y0 in range(0, W, tile_w):
+                blk = [(f * H + x) * W + y for x in range(x0, min(H, x0 + tile_h))
+                       for y in range(y0, min(W, y0 + tile_w))]
+                out += blk + [PAD] * (b - len(blk))
+    N = F * H * W
+    for s0 in range(0, text_tokens, b):
+        blk = list(range(N + s0, N + min(text_tokens, s0 + b)))
+        out += blk + [PAD] * (b - len(blk))
+    return np.asarray(out, dtype=np.int64)
+
+
+def block_tokens(perm, b: int, u: int) -> np.ndarray:
+    """Tokens of block u: positions [u*b, (u+1)*b) of the sequence order
+    (App. C: blocks of b consecutive positions), padding dropped."""
+    r = np.asarray(perm[u * b:(u + 1) * b], dtype=np.int64)
+    return r[r >= 0]
+
+
+def block_sizes(perm, b: int) -> np.ndarray:
+    """Number of tokens in each block of the sequence order (padding excluded)."""
+    perm = np.asarray(perm, dtype=np.int64)
+    nb = -(-perm.shape[0] // b)
+    return np.array([len(block_tokens(perm, b, u)) for u in range(nb)], dtype=np.int64)
 
 
 def block_bounds(N: int, b: int):
@@ -333,7 +379,8 @@ def block_mask_rows(n_raster, perm, b: int, F: int, H: int, W: int, gamma: float
     ``blocks``, from per-token squared radii ``n_raster`` (token order).
 
     ``perm`` is the sequence order (tile-major video tokens, then any text
-    tokens); blocks are b consecutive positions of it.  For a video query block
+    tokens, with PAD at empty positions of a padded layout); blocks are b
+    consecutive positions of it.  For a video query block
     u and a video key block v, every valid key column j of v gets the count c_j
     of valid queries i of u with M_ij = 1 (Eq. 15, or the 1-D test).
     C = {j : c_j > 0}, C_hi = {j : c_j > n_u / 3}.
@@ -344,27 +391,30 @@ def block_mask_rows(n_raster, perm, b: int, F: int, H: int, W: int, gamma: float
     any text token is retained in every row, and its own row retains every
     block (reading: a block mixing the last video tokens with the first text
     tokens counts as a text block, so every text key stays visible).
-    n_u is the number of valid queries of u; the high-coverage test is written
-    3 c_j > n_u.  Returns a bool array (len(blocks), NB).
+    n_u is the number of valid queries of u (padding is neither a query nor a
+    key); the high-coverage test is written 3 c_j > n_u.  Returns a bool array
+    (len(blocks), NB).
     """
     perm = np.asarray(perm, dtype=np.int64)
-    S = perm.shape[0]
+    P = perm.shape[0]
     N = F * H * W
-    nb = -(-S // b)
-    text_block = np.array([min(S, (v + 1) * b) > N for v in range(nb)])
+    nb = -(-P // b)
+    members = [block_tokens(perm, b, v) for v in range(nb)]
+    text_block = np.array([bool((m >= N).any()) for m in members])
+    valid = np.nonzero(perm >= 0)[0]
+    keys = perm[valid]
     out = np.zeros((len(blocks), nb), dtype=bool)
-    pad = nb * b - S
     for r, u in enumerate(blocks):
         if text_block[u]:
             out[r] = True
             continue
-        lo, hi = u * b, min((u + 1) * b, S)
-        rows = perm[lo:hi]
-        n_u = hi - lo
-        M = token_mask_rows(rows, np.asarray(n_raster)[rows], F, H, W, gamma, keys=perm,
+        rows = members[u]
+        n_u = len(rows)
+        M = token_mask_rows(rows, np.asarray(n_raster)[rows], F, H, W, gamma, keys=keys,
                             distance=distance)
-        c = M.sum(dim=0).numpy()                       # per key column, sequence order
-        c = np.concatenate([c, np.zeros(pad, dtype=c.dtype)]).reshape(nb, b)
+        c = np.zeros(nb * b, dtype=np.int64)           # per key column, by position
+        c[valid] = M.sum(dim=0).numpy()
+        c = c.reshape(nb, b)
         nonempty = (c > 0).sum(axis=1)
         high = (3 * c > n_u).sum(axis=1)
         if rule == "vote":
@@ -384,17 +434,16 @@ def masked_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, return_lse=F
     attends, with one softmax, to every key of every key block v with
     M[u, v] = 1, and to no other key.
 
-    q, k, v: (N, d) raster order.  Returns the output rows of the queries in
-    ``blocks`` as a dict {raster row index: o_i} packed as (rows, O)."""
+    q, k, v: (N, d) raster order; blocks are positions of ``perm`` as in
+    block_mask_rows (padding dropped).  Returns the output rows of the queries
+    in ``blocks`` as (rows, O)."""
     perm = np.asarray(perm, dtype=np.int64)
-    N = perm.shape[0]
     qt, kt, vt = _t(q), _t(k), _t(v)
     alpha = 1.0 / math.sqrt(qt.shape[1])
     rows_out, o_out, lse_out = [], [], []
     for r, u in enumerate(blocks):
-        rows = perm[u * b: min((u + 1) * b, N)]
-        keys = np.concatenate([perm[v * b: min((v + 1) * b, N)]
-                               for v in np.nonzero(mask_rows[r])[0]])
+        rows = block_tokens(perm, b, u)
+        keys = np.concatenate([block_tokens(perm, b, v) for v in np.nonzero(mask_rows[r])[0]])
         s = alpha * (qt[rows] @ kt[keys].T)
         m = s.max(dim=1, keepdim=True).values
         e = torch.exp(s - m)
@@ -421,16 +470,14 @@ def token_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, n_tok, F: int
     q, k, v: (S, d) token order.  Returns (rows, O) [and lse] for the queries of
     ``blocks``."""
     perm = np.asarray(perm, dtype=np.int64)
-    S = perm.shape[0]
     N = F * H * W
     qt, kt, vt = _t(q), _t(k), _t(v)
     alpha = 1.0 / math.sqrt(qt.shape[1])
     n_tok = np.asarray(n_tok)
     rows_out, o_out, lse_out = [], [], []
     for r, u in enumerate(blocks):
-        rows = perm[u * b: min((u + 1) * b, S)]
-        keys = np.concatenate([perm[v * b: min((v + 1) * b, S)]
-                               for v in np.nonzero(mask_rows[r])[0]])
+        rows = block_tokens(perm, b, u)
+        keys = np.concatenate([block_tokens(perm, b, v) for v in np.nonzero(mask_rows[r])[0]])
         video = rows < N
         M = torch.ones(len(rows), len(keys), dtype=torch.bool)
         if video.any():
@@ -450,13 +497,18 @@ def token_attention_rows(q, k, v, perm, b: int, blocks, mask_rows, n_tok, F: int
     return rows_out, np.concatenate(o_out)
 
 
-def retained_fraction(mask, N: int, b: int) -> float:
+def retained_fraction(mask, N: int, b: int, sizes=None) -> float:
     """Fraction of query-key interactions inside retained blocks,
-    sum over retained (u, v) of n_u n_v, over (heads * N^2).  mask: (..., NB, NB)."""
+    sum over retained (u, v) of n_u n_v, over (heads * N^2).  mask: (..., NB, NB).
+    sizes: tokens per block (block_sizes); default b per block with the last
+    one ragged (a packed order of N tokens)."""
     mask = np.asarray(mask, dtype=bool)
     nb = mask.shape[-1]
-    n = np.full(nb, b, dtype=np.int64)
-    n[-1] = N - (nb - 1) * b
+    if sizes is not None:
+        n = np.asarray(sizes, dtype=np.int64)
+    else:
+        n = np.full(nb, b, dtype=np.int64)
+        n[-1] = N - (nb - 1) * b
     per = np.einsum("...uv,u,v->...", mask.astype(np.int64), n, n)
     return float(np.sum(per) / (np.prod(mask.shape[:-2]) * N * N))
 

@@ -176,6 +176,117 @@ def test_full_tiles_are_contiguous_runs():
         assert x[r].max() - x[r].min() == 7 and y[r].max() - y[r].min() == 15
 
 
+# ------------------------------------------------- tile-aligned padded blocks
+def test_tile_aligned_order_golden(golden_dir):
+    want = np.array(_read_golden(golden_dir, "tile_aligned_order_F2_H3_W5_tile2x2_b4_T3.txt")[0],
+                    dtype=np.int64)
+    assert np.array_equal(O.tile_aligned_order(2, 3, 5, 2, 2, 4, text_tokens=3), want)
+
+
+@pytest.mark.parametrize("grid,tile,T", [((21, 30, 52), (8, 16), 0), ((3, 45, 80), (8, 16), 0),
+                                         ((2, 5, 9), (2, 4), 5), ((3, 11, 29), (8, 16), 130)])
+def test_tile_aligned_blocks_are_single_tiles(grid, tile, T):
+    """Every token appears exactly once; every video block lies in one frame and
+    one tile (its coordinates inside [x0, x0 + tile_h) x [y0, y0 + tile_w) of
+    one tile origin); tokens fill a prefix of the block; a text block holds
+    only text tokens; the block count is F * ceil(H/th) * ceil(W/tw) + ceil(T/b)."""
+    F, H, W = grid
+    th, tw = tile
+    b = th * tw
+    N = F * H * W
+    perm = O.tile_aligned_order(F, H, W, th, tw, b, text_tokens=T)
+    nb = perm.shape[0] // b
+    assert perm.shape[0] % b == 0
+    assert nb == F * (-(-H // th)) * (-(-W // tw)) + (-(-T // b))
+    valid = perm[perm >= 0]
+    assert np.array_equal(np.sort(valid), np.arange(N + T))
+    f, x, y = O.grid_coords(F, H, W)
+    for u in range(nb):
+        blk = perm[u * b:(u + 1) * b]
+        n = int((blk >= 0).sum())
+        assert n > 0 and (blk[:n] >= 0).all() and (blk[n:] == O.PAD).all()
+        r = blk[:n]
+        if (r >= N).any():
+            assert (r >= N).all()
+            continue
+        assert len(set(f[r])) == 1
+        assert len(set(x[r] // th)) == 1 and len(set(y[r] // tw)) == 1
+    assert np.array_equal(O.block_sizes(perm, b), [(perm[u * b:(u + 1) * b] >= 0).sum() for u in range(nb)])
+
+
+def test_tile_aligned_equals_tile_major_when_tiles_divide_the_frame():
+    """With tiles dividing the frame exactly there is no padding and the two
+    orders coincide."""
+    assert np.array_equal(O.tile_aligned_order(3, 16, 32, 8, 16, 128), O.tile_major_order(3, 16, 32, 8, 16))
+    assert np.array_equal(O.tile_aligned_order(4, 8, 8, 8, 8, 64), np.arange(256))
+
+
+def _brute_block_mask(n_raster, members, F, H, W, gamma, rule):
+    """Alg. 1 by loops over explicit token lists: c_j counts the queries i of u
+    with sqrt((x_i-x_j)^2 + (y_i-y_j)^2) <= sqrt(n_i) exp(-gamma |f_i - f_j|)."""
+    nb = len(members)
+    out = np.zeros((nb, nb), dtype=bool)
+    for u in range(nb):
+        for v in range(nb):
+            c = []
+            for j in members[v]:
+                fj, xj, yj = j // (H * W), (j // W) % H, j % W
+                cnt = 0
+                for i in members[u]:
+                    fi, xi, yi = i // (H * W), (i // W) % H, i % W
+                    if math.sqrt((xi - xj) ** 2 + (yi - yj) ** 2) <= \
+                            math.sqrt(n_raster[i]) * math.exp(-gamma * abs(fi - fj)):
+                        cnt += 1
+                c.append(cnt)
+            C = sum(1 for cj in c if cj > 0)
+            Chi = sum(1 for cj in c if 3 * cj > len(members[u]))
+            out[u, v] = (C > 0 and (10 * Chi > 6 * C if rule == "vote" else True)) or u == v
+    return out
+
+
+@pytest.mark.parametrize("rule", ["vote", "union"])
+def test_block_mask_on_padded_blocks_matches_brute_force(rule):
+    """Tile-aligned blocks with clipped edge tiles (2 x 5 x 6 grid, 2 x 4
+    tiles, b = 8: blocks of 8, 4, 8, 4 and 2 tokens per frame): the oracle's
+    mask equals Alg. 1 evaluated by loops over each block's token list, with
+    padding neither a query nor a key."""
+    F, H, W, th, tw, gamma = 2, 5, 6, 2, 4, 0.6
+    perm = O.tile_aligned_order(F, H, W, th, tw, th * tw)
+    nb = perm.shape[0] // 8
+    members = [O.block_tokens(perm, 8, u) for u in range(nb)]
+    assert sorted(len(m) for m in members[:6]) == [2, 4, 4, 4, 8, 8]
+    rng = np.random.default_rng(5)
+    n = rng.integers(0, 12, size=F * H * W)
+    got = O.block_mask_rows(n, perm, 8, F, H, W, gamma, range(nb), rule=rule)
+    assert np.array_equal(got, _brute_block_mask(n, members, F, H, W, gamma, rule))
+    assert 0 < got.sum() < nb * nb
+
+
+def test_masked_attention_on_padded_blocks():
+    """Padded blocks: a full mask gives dense attention over every token; the
+    identity mask gives attention restricted to each tile's own tokens."""
+    w = synth.workload("tiny")
+    q, k, v = (synth.to_f64(a[0, 0], w.dtype) for a in synth.generate(w))
+    perm = O.tile_aligned_order(4, 8, 8, 3, 8, 24)           # 8 rows = 3 + 3 + 2: partial tiles
+    nb = perm.shape[0] // 24
+    rows, o = O.masked_attention_rows(q, k, v, perm, 24, range(nb), np.ones((nb, nb), bool))
+    assert np.array_equal(np.sort(rows), np.arange(256))
+    assert np.abs(o - O.dense_attention(q[rows], k, v)).max() < 1e-12
+    rows, o = O.masked_attention_rows(q, k, v, perm, 24, [2, 5], np.eye(nb, dtype=bool)[[2, 5]])
+    at = 0
+    for u in (2, 5):
+        idx = O.block_tokens(perm, 24, u)
+        want = O.dense_attention(q[idx], k[idx], v[idx])
+        assert np.abs(o[at:at + len(idx)] - want).max() < 1e-12
+        at += len(idx)
+
+
+def test_retained_fraction_with_block_sizes():
+    sizes = np.array([8, 4, 2])
+    eye = np.eye(3, dtype=bool)[None]
+    assert abs(O.retained_fraction(eye, 14, 8, sizes=sizes) - (64 + 16 + 4) / 196) < 1e-15
+
+
 # ------------------------------------------------------------------ radius
 def test_threshold_golden(golden_dir):
     for gamma, n, *want in _read_golden(golden_dir, "thresholds.txt"):
