@@ -134,12 +134,24 @@ class MaskSource:
         return "own entropies"
 
 
-class MaskBuffers:
-    """Device buffers of one mask (radii, mask, lists, order) for a plan."""
+def layout_block_sizes(tra, plan):
+    """Tokens per block of a plan's block layout (None for the packed layout,
+    whose blocks are full but the last), from the library's host tables."""
+    if plan.cfg.block_layout != "tiles":
+        return None
+    import torch
+    blocks = tra.tra_plan_host_tables(plan.cfg)[3]
+    return torch.from_numpy((blocks[:, 6] + blocks[:, 9]).astype(np.float64))
 
-    def __init__(self, plan, B, Ha, N, dev):
+
+class MaskBuffers:
+    """Device buffers of one mask (radii, mask, lists, order) for a plan, and
+    the tokens per block of its layout (None: packed)."""
+
+    def __init__(self, plan, B, Ha, N, dev, sizes=None):
         import torch
         NB = plan.n_blocks
+        self.sizes = sizes
         self.H = torch.empty(B, Ha, N, dtype=torch.float32, device=dev)
         self.rad = torch.empty(B, Ha, N, dtype=torch.int32, device=dev)
         self.mask = torch.empty(B, Ha, NB, NB, dtype=torch.uint8, device=dev)
@@ -148,13 +160,17 @@ class MaskBuffers:
         self.order = torch.empty(plan.rows, dtype=torch.int32, device=dev)
 
 
-def kept_fraction(mask, N, b, d):
-    """Executed FLOPs of a mask (R15) and their fraction of the dense call's,
-    computed on the device."""
+def kept_fraction(mask, N, b, d, sizes=None):
+    """Executed FLOPs of a mask (R15: on token pairs, padding excluded) and
+    their fraction of the dense call's, computed on the device.  sizes: tokens
+    per block (default: a packed layout of N tokens)."""
     import torch
     B, Ha, NB, _ = mask.shape
-    nvec = torch.full((NB,), float(b), dtype=torch.float64, device=mask.device)
-    nvec[-1] = N - (NB - 1) * b
+    if sizes is None:
+        nvec = torch.full((NB,), float(b), dtype=torch.float64, device=mask.device)
+        nvec[-1] = N - (NB - 1) * b
+    else:
+        nvec = sizes.to(device=mask.device, dtype=torch.float64)
     fl = 4.0 * d * float(torch.einsum("bhuv,u,v->", mask.to(torch.float64), nvec, nvec))
     return fl / (4.0 * d * N * N * B * Ha), fl
 
@@ -172,7 +188,7 @@ def fit_mask_source(tra, plan, w, H_own, mb, kind, target):
         src.apply(mb.H)
         tra.tra_budget_radius(plan, mb.H, None, mb.rad)
         tra.tra_build_block_mask(plan, mb.rad, mb.mask, mb.cnt, mb.cols, None)
-        return kept_fraction(mb.mask, N, w.block, d)[0]
+        return kept_fraction(mb.mask, N, w.block, d, mb.sizes)[0]
 
     if kind == "own":
         src = MaskSource("own")
@@ -214,7 +230,7 @@ def density_sweep(tra, plan, w, q, k, v, H_own, dense_ms, targets, iters=3):
     and both row schedules (the kernel's per-XCD row queues, and the mask
     builder's heaviest-first order).  Q, K, V are the workload's own."""
     B, Ha, N, d = q.shape
-    mb = MaskBuffers(plan, B, Ha, N, q.device)
+    mb = MaskBuffers(plan, B, Ha, N, q.device, sizes=layout_block_sizes(tra, plan))
     import torch
     o = torch.empty_like(q)
     rows = []
@@ -222,7 +238,7 @@ def density_sweep(tra, plan, w, q, k, v, H_own, dense_ms, targets, iters=3):
         for target in targets:
             src = fit_mask_source(tra, plan, w, H_own, mb, kind, target)
             tra.tra_build_block_mask(plan, mb.rad, mb.mask, mb.cnt, mb.cols, mb.order)
-            rho, fl = kept_fraction(mb.mask, N, w.block, d)
+            rho, fl = kept_fraction(mb.mask, N, w.block, d, mb.sizes)
             cnt = mb.cnt.reshape(-1).double()
             row = {"masks": kind, "target": target, "source": src.describe(w.tau),
                    "retained_fraction": round(rho, 5),
@@ -244,6 +260,39 @@ def density_sweep(tra, plan, w, q, k, v, H_own, dense_ms, targets, iters=3):
             log(f"density {kind} {target}: rho {rho:.4f} sparse none {row['sparse_ms_order_none']:.3f} ms "
                 f"heavy {row['sparse_ms_order_heavy']:.3f} ms")
     return rows
+
+
+def layout_comparison(tra, w, q, k, v, H_own, src, dense_ms, iters=3):
+    """The same radii (the step's mask source) through both block layouts:
+    packed blocks of b consecutive tile-major positions, and tile-aligned
+    padded blocks (one tile of one frame each).  Per layout: blocks per head,
+    retained fraction on token pairs (R15) and with padding counted, mask,
+    block-sparse and token-level times."""
+    import torch
+    B, Ha, N, d = q.shape
+    b = w.block
+    out = {}
+    for layout in ("packed", "tiles"):
+        plan = tra.Plan(tra.Config.from_workload(w, block_layout=layout))
+        mb = MaskBuffers(plan, B, Ha, N, q.device, sizes=layout_block_sizes(tra, plan))
+        mb.H.copy_(H_own)
+        src.apply(mb.H)
+        tra.tra_budget_radius(plan, mb.H, None, mb.rad)
+        mask_ms = _time_call(lambda: tra.tra_build_block_mask(plan, mb.rad, mb.mask, mb.cnt, mb.cols, None),
+                             iters)
+        rho, fl = kept_fraction(mb.mask, N, b, d, mb.sizes)
+        padded = float(mb.mask.double().sum()) * b * b / (B * Ha * float(N) * N)
+        o = torch.empty_like(q)
+        sp = _time_call(lambda: tra.tra_sparse_attention(plan, q, k, v, mb.cnt, mb.cols, None, o), iters)
+        tok = _time_call(lambda: tra.tra_token_attention(plan, q, k, v, mb.rad, mb.cnt, mb.cols, None, o), iters)
+        out[layout] = {"n_blocks": plan.n_blocks, "retained_fraction": round(rho, 5),
+                       "retained_fraction_with_padding": round(padded, 5), "mask_ms": round(mask_ms, 4),
+                       "sparse_ms": round(sp, 4), "sparse_tflops": round(fl / (sp * 1e-3) / 1e12, 2),
+                       "eta": round(rho * dense_ms / sp, 4), "token_level_ms": round(tok, 4),
+                       "token_level_vs_block": round(sp / tok, 4)}
+        log(f"layout {layout}: {out[layout]}")
+        del mb, plan, o
+    return out
 
 
 def library_gemm_reference(n=16384, iters=5):
@@ -528,6 +577,9 @@ def main():
                          "entropies unchanged (own: every block kept on these generators)")
     ap.add_argument("--density", type=float, default=0.15,
                     help="retained fraction the entropy / uniform masks are fitted to (Table 1: 0.09-0.19)")
+    ap.add_argument("--block-layout", choices=["packed", "tiles"], default="packed",
+                    help="blocks of the mask and the sparse call: packed tile-major runs, or tile-aligned "
+                         "padded blocks (one tile of one frame each)")
     ap.add_argument("--order", choices=["heavy", "none"], default="none",
                     help="row schedule of the sparse kernel: heaviest-first list or the per-XCD row queues")
     ap.add_argument("--dense-iters", type=int, default=3)
@@ -580,11 +632,11 @@ def main():
     else:
         conv = lambda a: torch.from_numpy(a).cuda()
     q, k, v = conv(q_np), conv(k_np), conv(v_np)
-    plan = tra.Plan(tra.Config.from_workload(w))
+    plan = tra.Plan(tra.Config.from_workload(w, block_layout=args.block_layout))
     B, Ha, N, d = q.shape
     NB = plan.n_blocks
     dev = q.device
-    mb = MaskBuffers(plan, B, Ha, N, dev)
+    mb = MaskBuffers(plan, B, Ha, N, dev, sizes=layout_block_sizes(tra, plan))
     H, rad, mask, cnt, cols, order = mb.H, mb.rad, mb.mask, mb.cnt, mb.cols, mb.order
     o_sp = torch.empty_like(q)
     o_d = torch.empty_like(q)
@@ -657,7 +709,7 @@ def main():
     token_ms = _time_call(lambda: tra.tra_token_attention(plan, q, k, v, rad, cnt, cols, None, o_sp),
                           max(1, args.dense_iters))
 
-    rho, flops = kept_fraction(mask, N, w.block, d)
+    rho, flops = kept_fraction(mask, N, w.block, d, mb.sizes)
     cnt_rows = cnt.reshape(-1).double()
     dense_flops = 4.0 * d * N * N * B * Ha
     sp = stage_ms["sparse"]
@@ -670,7 +722,7 @@ def main():
     rad_bytes = 8 * B * Ha * N
     mask_bytes = 4 * B * Ha * N + B * Ha * NB * NB * 5 + 8 * B * Ha * NB
     headline = args.workload == "wan14b_720p" and args.masks == "entropy" and args.density == 0.15 \
-        and args.order == "none"
+        and args.order == "none" and args.block_layout == "packed"
     trace = profiled("trace") if headline else None
     counters = profiled("counters") if headline else None
     roofline = {
@@ -712,7 +764,7 @@ def main():
                          f"tau {w.tau}, gamma {w.gamma}, vote mask; masks from {masks_desc}"),
             "global_batch": w.batch, "seq_len": N, "parallelism": "single GPU",
             "masks": args.masks, "mask_source": src.describe(w.tau), "density_target": args.density,
-            "row_schedule": args.order,
+            "row_schedule": args.order, "block_layout": args.block_layout,
         },
         "paper_context": ("the paper reports 1.56-2.05x end-to-end video generation speedups at 9-19 % "
                           "retained interactions on one NVIDIA H200 (whole pipeline, not a per-call "
@@ -740,9 +792,9 @@ def main():
     }
     if not args.no_extras and w.dtype == "bf16":
         log("all-kept call: masks from the workload's own entropies")
-        mb_own = MaskBuffers(plan, B, Ha, N, dev)
+        mb_own = MaskBuffers(plan, B, Ha, N, dev, sizes=mb.sizes)
         fit_mask_source(tra, plan, w, H_own, mb_own, "own", None)
-        rho1, fl1 = kept_fraction(mb_own.mask, N, w.block, d)
+        rho1, fl1 = kept_fraction(mb_own.mask, N, w.block, d, mb.sizes)
         ms1 = _time_call(lambda: tra.tra_sparse_attention(plan, q, k, v, mb_own.cnt, mb_own.cols, None, o_sp),
                          max(3, args.dense_iters))
         out["all_kept"] = {"masks": "own entropies", "retained_fraction": round(rho1, 5),
@@ -754,6 +806,8 @@ def main():
         g = library_gemm_reference()
         g["sparse_over_gemm"] = round(achieved / g["tflops"], 4)
         out["library_gemm_reference"] = g
+        log("block layouts on the step's radii: packed and tile-aligned padded blocks")
+        out["block_layouts"] = layout_comparison(tra, w, q, k, v, H_own, src, dn)
         log("density sweep at the paper's retained fractions (shifted entropies and uniform budgets)")
         out["density_sweep"] = density_sweep(tra, plan, w, q, k, v, H_own, dn, [0.09, 0.15, 0.19])
         log("budget mapping and distance options")

@@ -35,10 +35,12 @@
  * The library applies the tile-major token order of Sec. 3.3 internally: each
  * frame is cut into tile_h x tile_w tiles (edge tiles clipped), tokens are
  * listed frame by frame, tile by tile, row-major inside a tile; text tokens
- * follow the video tokens unchanged.  Block u is positions
- * [u*block, min((u+1)*block, S)) of that order and NB = ceil(S / block) (App. C).
- * A block holding any text token is a text block.  Block-level arrays use row
- * index
+ * follow the video tokens unchanged.  With the packed block layout (default)
+ * block u is positions [u*block, min((u+1)*block, S)) of that order and
+ * NB = ceil(S / block) (App. C).  With tile-aligned padded blocks
+ * (TRA_BLOCKS_TILES) every video block is one whole tile of one frame, padded
+ * when the frame edge clips the tile (see tra_block_layout).  A block holding
+ * any text token is a text block.  Block-level arrays use row index
  * r = (b*heads + h)*NB + u:
  *   mask [batch][heads][NB][NB] uint8 (1 = retained),
  *   cnt  [batch][heads][NB]     int32 (retained key blocks of row r),
@@ -122,6 +124,24 @@ typedef enum { TRA_BUDGET_UNIFORM = 0, TRA_BUDGET_LOGNORMAL = 1 } tra_budget_map
  * 1-D radius (pi/2) n phi(delta), n the squared 2-D radius. */
 typedef enum { TRA_DIST_2D = 0, TRA_DIST_1D = 1 } tra_distance;
 
+/* Block layout of the block mask and of the block-sparse and token-level
+ * calls (the blocks their mask, cnt, cols and order refer to).
+ * PACKED: block u is positions [u b, (u+1) b) of the tile-major order, so a
+ *   block may hold parts of two tiles, or of two frames; NB = ceil(S / b).
+ * TILES: tile-aligned padded blocks.  Every video block is exactly one
+ *   tile_h x tile_w tile of one frame (tile_h * tile_w must equal b): frames
+ *   in order, tiles in tile-row-major order, tokens row-major inside the tile.
+ *   A tile clipped by the frame edge fills the first positions of its block;
+ *   the rest are padding, neither queries nor keys.  Text tokens follow in
+ *   blocks of b, the last one padded.  NB = F ceil(H / tile_h) ceil(W /
+ *   tile_w) + ceil(T / b).  A block then has the smallest spatial footprint b
+ *   tokens can have, so fewer of its keys lie outside a query's radius: App. D
+ *   names that in-block work as the block-granular method's main limitation.
+ *   bf16 plans only.
+ * tra_entropy and tra_dense_attention are defined over tokens and give the
+ * same results under both layouts. */
+typedef enum { TRA_BLOCKS_PACKED = 0, TRA_BLOCKS_TILES = 1 } tra_block_layout;
+
 typedef struct tra_config {
   int32_t batch;     /* >= 1                                                  */
   int32_t heads;     /* >= 1                                                  */
@@ -137,6 +157,7 @@ typedef struct tra_config {
   int32_t budget_map;   /* tra_budget_map                                     */
   int32_t distance;     /* tra_distance                                       */
   int32_t text_tokens;  /* T >= 0 text tokens after the video tokens          */
+  int32_t block_layout; /* tra_block_layout                                   */
   double tau;        /* target attention mass, 0 < tau < 1 (paper: 0.9)      */
   double gamma;      /* temporal decay rate of phi(delta) = exp(-gamma delta),
                         gamma >= 0 (Eq. 10; 0.6 Wan, 0.95 HunyuanVideo)       */
@@ -166,18 +187,21 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out);
 tra_status tra_plan_destroy(tra_plan plan);
 
 /* n_tokens = S = F*H*W + text_tokens (the token count of every per-token
- * tensor), NB = ceil(S / block), n_cap as above.  Any output may be NULL. */
+ * tensor), NB of the plan's block layout, n_cap as above.  Any output may be
+ * NULL. */
 tra_status tra_plan_dims(tra_plan plan, int32_t* n_tokens, int32_t* n_blocks,
                          int32_t* n_cap);
 
 /* Host-only (no device needed): the plan's tables for cfg, for inspection.
- * perm[S]: token index (raster for video, N + t for text token t) of the
- *          token at position p of the tile-major order.
+ * perm[P]: token index (raster for video, N + t for text token t) of the
+ *          token at position p of the block layout's order, -1 at a padding
+ *          position; P = S for the packed layout, NB * block for tiles.
  * thr[(n_cap+1) * F]: thr[n*F + delta] (2-D, squared).
  * thr1[(n_cap+1) * F]: thr1[n*F + delta] = floor((pi/2) n exp(-gamma delta)).
  * blocks[NB * 10]: per block {f_min, f_max, x_min, x_max, y_min, y_max,
  *                 n_video, r_min, r_max, n_text} over its video tokens (r the
- *                 raster index) and the count of its text tokens.
+ *                 raster index) and the count of its text tokens; a block's
+ *                 tokens fill its first n_video + n_text positions.
  * Any array pointer may be NULL; *n_cap_out (may be NULL) gets n_cap. */
 tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* thr,
                                 int32_t* thr1, int32_t* blocks, int32_t* n_cap_out);
@@ -298,8 +322,8 @@ tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
  * covers no listed key gets o = 0, lse = -inf.  Whole 128-key tiles that none
  * of a wave's 32 queries covers are skipped.  bf16 plans need every threshold
  * below 65536 (n_cap <= 65535 for 2-D, floor(pi/2 n_cap) <= 65535 for 1-D)
- * and at least one block of video tokens per frame (H*W >= block), else
- * TRA_ERR_UNSUPPORTED.  workspace: TRA_CALL_TOKEN. */
+ * and, with the packed layout, at least one block of video tokens per frame
+ * (H*W >= block), else TRA_ERR_UNSUPPORTED.  workspace: TRA_CALL_TOKEN. */
 tra_status tra_token_attention(tra_plan plan, const void* q, const void* k, const void* v,
                                const int32_t* radius_sq, const int32_t* cnt,
                                const int32_t* cols, const int32_t* order, void* o,

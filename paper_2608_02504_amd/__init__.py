@@ -27,7 +27,7 @@ import numpy as np
 __all__ = [
     "LIB_PATH", "TRA_RADIUS_FULL", "TraError", "Config", "Plan", "lib", "library_loaded",
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
-    "tra_workspace_size", "TRA_CALL_ENTROPY", "TRA_CALL_BLOCK_MASK", "TRA_CALL_SPARSE",
+    "tra_workspace_size", "TRA_BLOCKS_PACKED", "TRA_BLOCKS_TILES", "TRA_CALL_ENTROPY", "TRA_CALL_BLOCK_MASK", "TRA_CALL_SPARSE",
     "TRA_CALL_TOKEN", "TRA_CALL_DENSE", "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
     "tra_sparse_attention", "tra_token_attention", "tra_dense_attention", "tra_version",
     "EXPORTED_SYMBOLS",
@@ -39,6 +39,8 @@ TRA_BF16, TRA_FP32 = 0, 1
 TRA_MASK_VOTE, TRA_MASK_UNION = 0, 1
 TRA_BUDGET_UNIFORM, TRA_BUDGET_LOGNORMAL = 0, 1
 TRA_DIST_2D, TRA_DIST_1D = 0, 1
+TRA_BLOCKS_PACKED, TRA_BLOCKS_TILES = 0, 1
+_LAYOUT = {"packed": TRA_BLOCKS_PACKED, "tiles": TRA_BLOCKS_TILES}
 TRA_CALL_ENTROPY, TRA_CALL_BLOCK_MASK, TRA_CALL_SPARSE, TRA_CALL_TOKEN, TRA_CALL_DENSE = range(5)
 _CALLS = (TRA_CALL_ENTROPY, TRA_CALL_BLOCK_MASK, TRA_CALL_SPARSE, TRA_CALL_TOKEN, TRA_CALL_DENSE)
 _BUDGET = {"uniform": TRA_BUDGET_UNIFORM, "lognormal": TRA_BUDGET_LOGNORMAL}
@@ -64,7 +66,8 @@ class TraError(RuntimeError):
 class _Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "batch", "heads", "frames", "height", "width", "head_dim", "block",
-        "tile_h", "tile_w", "dtype", "rule", "budget_map", "distance", "text_tokens")] + [
+        "tile_h", "tile_w", "dtype", "rule", "budget_map", "distance", "text_tokens",
+        "block_layout")] + [
         ("tau", ctypes.c_double), ("gamma", ctypes.c_double)]
 
 
@@ -87,6 +90,7 @@ class Config:
     budget: str = "uniform"   # "uniform" (Eq. 8) or "lognormal" (App. A.2)
     distance: str = "2d"      # "2d" (Eq. 15) or "1d" (sequence-distance ablation)
     text_tokens: int = 0      # text tokens after the video tokens (joint attention)
+    block_layout: str = "packed"  # "packed" or "tiles" (tile-aligned padded blocks)
 
     @property
     def n_video(self) -> int:
@@ -98,7 +102,15 @@ class Config:
 
     @property
     def n_blocks(self) -> int:
+        if self.block_layout == "tiles":
+            return (self.frames * -(-self.height // self.tile_h) * -(-self.width // self.tile_w)
+                    + -(-self.text_tokens // self.block))
         return -(-self.n_tokens // self.block)
+
+    @property
+    def n_positions(self) -> int:
+        """Positions of the block layout's order (the length of the plan's perm)."""
+        return self.n_blocks * self.block if self.block_layout == "tiles" else self.n_tokens
 
     def to_c(self) -> _Config:
         return _Config(self.batch, self.heads, self.frames, self.height, self.width,
@@ -106,7 +118,7 @@ class Config:
                        TRA_BF16 if self.dtype == "bf16" else TRA_FP32 if self.dtype == "fp32" else 99,
                        TRA_MASK_VOTE if self.rule == "vote" else TRA_MASK_UNION if self.rule == "union" else 99,
                        _BUDGET.get(self.budget, 99), _DIST.get(self.distance, 99), self.text_tokens,
-                       self.tau, self.gamma)
+                       _LAYOUT.get(self.block_layout, 99), self.tau, self.gamma)
 
     @classmethod
     def from_workload(cls, w, **kw) -> "Config":
@@ -226,12 +238,12 @@ def tra_plan_dims(plan: Plan):
 
 
 def tra_plan_host_tables(cfg: Config):
-    """Host-only tables of cfg:
-    (perm[S], thr[(n_cap+1), F], thr1[(n_cap+1), F], blocks[NB, 10], n_cap)."""
+    """Host-only tables of cfg: (perm[P], thr[(n_cap+1), F], thr1[(n_cap+1), F],
+    blocks[NB, 10], n_cap); P = cfg.n_positions, perm -1 at padding positions."""
     c = cfg.to_c()
     cap = ctypes.c_int32()
     _check(lib().tra_plan_host_tables(ctypes.byref(c), None, None, None, None, ctypes.byref(cap)))
-    perm = np.empty(cfg.n_tokens, dtype=np.int32)
+    perm = np.empty(cfg.n_positions, dtype=np.int32)
     thr = np.empty((cap.value + 1, cfg.frames), dtype=np.int32)
     thr1 = np.empty((cap.value + 1, cfg.frames), dtype=np.int32)
     blocks = np.empty((cfg.n_blocks, 10), dtype=np.int32)

@@ -90,7 +90,8 @@ WsLayout ws_layout(const tra_plan_s& p, int call) {
   if (call == TRA_CALL_BLOCK_MASK) {
     L.sort = take((size_t)p.sort_ws_elems * sizeof(int32_t));
   } else if (p.cfg.dtype == TRA_BF16) {
-    const size_t kv = (size_t)p.cfg.batch * p.cfg.heads * p.n_pad * p.cfg.head_dim * sizeof(uint16_t);
+    const size_t kv =
+        (size_t)p.cfg.batch * p.cfg.heads * std::max(p.n_pad, p.n_pada) * p.cfg.head_dim * sizeof(uint16_t);
     L.kt = take(kv);
     L.vt = take(kv);
     L.ctr = take(tra::kRowCounters * sizeof(int32_t));
@@ -156,7 +157,7 @@ tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* t
     tra::HostTables t;
     tra::build_host_tables(*cfg, &t, perm != nullptr, thr != nullptr, thr1 != nullptr,
                            blocks != nullptr);
-    if (perm) std::memcpy(perm, t.perm.data(), t.perm.size() * sizeof(int32_t));
+    if (perm) std::memcpy(perm, t.perm.data(), t.perm.size() * sizeof(int32_t));  // P entries
     if (thr) std::memcpy(thr, t.thr.data(), t.thr.size() * sizeof(int32_t));
     if (thr1) std::memcpy(thr1, t.thr1.data(), t.thr1.size() * sizeof(int32_t));
     if (blocks) std::memcpy(blocks, t.blocks.data(), t.blocks.size() * sizeof(int32_t));
@@ -174,8 +175,10 @@ tra_status tra_plan_destroy(tra_plan p) {
   int prev = -1;
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(p->device);
+  if (p->d_perma != p->d_perm) (void)hipFree(p->d_perma);
   (void)hipFree(p->d_perm);
   (void)hipFree(p->d_coord);
+  (void)hipFree(p->d_bcount);
   (void)hipFree(p->d_thr);
   (void)hipFree(p->d_thr1);
   (void)hipFree(p->d_blocks);
@@ -221,6 +224,10 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
     // chunk histograms over keys 0..NB, plus one total slot
     p->sort_ws_elems = (int64_t)(t.NB + 1) * p->sort_chunks + 1;
     p->n_pad = t.NB * cfg->block;
+    const bool tiles = cfg->block_layout == TRA_BLOCKS_TILES;
+    p->NBa = tiles ? (t.S + cfg->block - 1) / cfg->block : t.NB;
+    p->n_pada = p->NBa * cfg->block;
+    p->rowsa = cfg->batch * cfg->heads * p->NBa;
     // the largest threshold: thr[n][0] = n, thr1[n][0] = floor(pi/2 n), at n = n_cap
     p->thr_max = one_d ? t.thr1[(size_t)t.n_cap * cfg->frames] : t.n_cap;
 
@@ -229,14 +236,25 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       if (err != hipSuccess) return err;
       return hipMemcpy(*dst, src.data(), src.size() * sizeof(int32_t), hipMemcpyHostToDevice);
     };
-    if ((e = upload(&p->d_perm, t.perm)) != hipSuccess ||
-        (e = upload(&p->d_coord, t.coord)) != hipSuccess ||
+    // position tables padded to whole blocks: -1 (no token) / 0 past the order's end
+    std::vector<int32_t> perm_pad = t.perm, coord_pad = t.coord, bcount(t.NB);
+    perm_pad.resize(p->n_pad, -1);
+    coord_pad.resize(p->n_pad, 0);
+    for (int u = 0; u < t.NB; ++u)
+      bcount[u] = t.blocks[(size_t)u * tra::kBlockInfo + 6] + t.blocks[(size_t)u * tra::kBlockInfo + 9];
+    std::vector<int32_t> perma_pad = t.perm_attn;
+    if (tiles) perma_pad.resize(p->n_pada, -1);
+    if ((e = upload(&p->d_perm, perm_pad)) != hipSuccess ||
+        (e = upload(&p->d_coord, coord_pad)) != hipSuccess ||
+        (e = upload(&p->d_bcount, bcount)) != hipSuccess ||
+        (tiles && (e = upload(&p->d_perma, perma_pad)) != hipSuccess) ||
         (e = upload(&p->d_thr, t.thr)) != hipSuccess ||
         (e = upload(&p->d_blocks, t.blocks)) != hipSuccess ||
         (one_d && (e = upload(&p->d_thr1, t.thr1)) != hipSuccess)) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
     }
+    if (!tiles) p->d_perma = p->d_perm;
     if ((e = hipMalloc((void**)&p->d_cap_count, (size_t)std::max(p->N, 1) * sizeof(int32_t))) != hipSuccess ||
         (e = tra::fill_cap_counts(*p, p->d_cap_count, nullptr)) != hipSuccess ||
         (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
@@ -289,6 +307,13 @@ static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a, vo
                                 void* stream, const char* what) {
   tra_plan_s bound;
   TRA_TRY(bind_workspace(p, call, true, ws, ws_bytes, &bound));
+  if (call == TRA_CALL_ENTROPY || call == TRA_CALL_DENSE) {
+    // defined over tokens: run on the packed order whatever the block layout
+    bound.NB = p->NBa;
+    bound.n_pad = p->n_pada;
+    bound.rows = p->rowsa;
+    bound.d_perm = p->d_perma;
+  }
   hipError_t e = p->cfg.dtype == TRA_BF16
                      ? tra::launch_attention_bf16(bound, a, (hipStream_t)stream)
                      : tra::launch_attention_f32(bound, a, (hipStream_t)stream);
@@ -394,7 +419,7 @@ tra_status tra_token_attention(tra_plan p, const void* q, const void* k, const v
   if (p->cfg.dtype == TRA_BF16) {
     if (p->thr_max > 65535)
       return fail(TRA_ERR_UNSUPPORTED, "token attention on bf16 plans needs every threshold below 65536");
-    if (p->cfg.height * p->cfg.width < p->cfg.block)
+    if (p->cfg.block_layout == TRA_BLOCKS_PACKED && p->cfg.height * p->cfg.width < p->cfg.block)
       return fail(TRA_ERR_UNSUPPORTED, "token attention on bf16 plans needs height * width >= block");
   }
   tra::AttnArgs a{q, k, v, o, lse, nullptr, cnt, cols, order, true, radius_sq};

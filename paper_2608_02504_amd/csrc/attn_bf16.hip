@@ -11,8 +11,8 @@
 //
 // Layout pre-pass
 //   K and V are first gathered into tile-major order (Sec. 3.3: tokens of a
-//   spatial tile become contiguous) in the plan's workspace, one 128-token key
-//   block = one contiguous tile, rows past N zero-filled: K as 128 rows x D,
+//   spatial tile become contiguous) in the call's workspace, one 128-token key
+//   block = one contiguous tile, padding positions zero-filled: K as 128 rows x D,
 //   V transposed (D rows x 128 keys), so that both matrix operands are read
 //   from LDS with plain 16-byte reads.  The attention loop then addresses
 //   tiles affinely.  Q is gathered and O scattered through the same
@@ -97,7 +97,7 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // ------------------------------------------------------------ layout pre-pass
-// kt[bh][p][:] = k[bh][perm[p]][:] for p < N, 0 for N <= p < n_pad.
+// kt[bh][p][:] = k[bh][perm[p]][:], 0 where perm[p] < 0 (a padding position).
 __global__ __launch_bounds__(256) void gather_k_kernel(const uint4* __restrict__ k,
                                                        uint4* __restrict__ kt,
                                                        const int32_t* __restrict__ perm, int N,
@@ -108,11 +108,12 @@ __global__ __launch_bounds__(256) void gather_k_kernel(const uint4* __restrict__
   const long long bh = idx / per_head;
   const long long rem = idx - bh * per_head;
   const int p = (int)(rem / ch), c = (int)(rem - (long long)p * ch);
-  kt[idx] = p < N ? k[(bh * N + perm[p]) * ch + c] : make_uint4(0, 0, 0, 0);
+  const int tok = perm[p];
+  kt[idx] = tok >= 0 ? k[(bh * N + tok) * ch + c] : make_uint4(0, 0, 0, 0);
 }
 
 // V transposed per key block, tile-major: for tile-major position p = 128 b + j,
-// vt[bh][b][d][j] = v[bh][perm[p]][d] (0 for N <= p < n_pad), so key block b of a
+// vt[bh][b][d][j] = v[bh][perm[p]][d] (0 at a padding position), so key block b of a
 // head is one contiguous D x 128 tile with the key index fastest.  One
 // workgroup per 64 tokens of one head, through LDS.
 template <int D>
@@ -126,7 +127,8 @@ __global__ __launch_bounds__(256) void gather_vt_kernel(const uint16_t* __restri
   for (int i = t; i < TOK * CH; i += 256) {
     const int j = i / CH, c = i - j * CH;
     uint4 x = make_uint4(0, 0, 0, 0);
-    if (p0 + j < N) x = *(const uint4*)(v + ((size_t)bh * N + perm[p0 + j]) * D + c * 8);
+    const int tok = perm[p0 + j];
+    if (tok >= 0) x = *(const uint4*)(v + ((size_t)bh * N + tok) * D + c * 8);
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -690,8 +692,9 @@ __device__ __forceinline__ void bf16_row(
   const uint32_t v_off = vt_lane_off(wave, lane);
 
   const int qpos = u * kBQ + wave * 32 + col;
-  const bool qvalid = qpos < N;
-  const int qrow = qvalid ? perm[qpos] : 0;
+  const int qtok = perm[qpos];  // -1 at a padding position
+  const bool qvalid = qtok >= 0;
+  const int qrow = qvalid ? qtok : 0;
   bf16x8 qf[G::QK_STEPS];
   {
     const uint4* src = (const uint4*)(q + head_off + (size_t)qrow * D);
@@ -712,7 +715,7 @@ __device__ __forceinline__ void bf16_row(
   [[maybe_unused]] bool tq_all = true;
   const int qi = wave * 32 + col;
   if constexpr (TOK != 0) {
-    if (qvalid && qpos < tk.Nv) {
+    if (qvalid && qrow < tk.Nv) {
       int n = tk.radius_sq[(size_t)bh * N + qrow];
       tq_all = n > tk.n_cap;
       n = max(n, 0);
@@ -793,9 +796,11 @@ __device__ __forceinline__ void bf16_row(
       // a wave all of whose queries cover every key skips the key test
       bool wave_skip = false, wave_test = false;
       int t_lo = INT_MAX, t_hi = INT_MAX;
+      int n_keys = N - b_cur * kBK;  // keys of the block holding a token (its first n_keys)
       if constexpr (TOK != 0) {
         const int32_t* bi = tk.binfo + (size_t)b_cur * kBlockInfo;
         const int fmin = bi[0], fmax = bi[1], n_video = bi[6], n_text = bi[9];
+        n_keys = n_video + n_text;
         bool none = !qvalid, all = true;
         if (qvalid && n_video > 0 && !tq_all) {
           t_lo = thrq[qi * tk.F + abs(tq_f - fmin)];
@@ -834,7 +839,7 @@ __device__ __forceinline__ void bf16_row(
             token_mask<TOK>(s, ki, half, tq_word, t_lo, t_hi);
           }
         }
-        if (N - b_cur * kBK < kBK) mask_tail(s, N - b_cur * kBK, half);
+        if (n_keys < kBK) mask_tail(s, n_keys, half);
         sc = tile_max<ENT>(s, scale_log2, st);
         float lsum = 0.f, asum = 0.f, lrsum = 0.f;
 #pragma unroll
@@ -973,8 +978,8 @@ __device__ __forceinline__ void k64_row(
     int r, int beg, int end, int slot, uint8_t* smemK, uint8_t* smemV, int32_t* smemCols,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
     uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ cols, int N, int n_pad, int NB, float scale_log2,
-    float* __restrict__ part, float* __restrict__ pstats) {
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ bcount, int N, int n_pad, int NB,
+    float scale_log2, float* __restrict__ part, float* __restrict__ pstats) {
   using G = Geo<D>;
   constexpr int KT_BYTES = kKT * D * 2;            // one 64-key tile of K or V^T
   constexpr int STEPS = KT_BYTES / 4096;           // 4 KB copy steps per tile
@@ -994,8 +999,9 @@ __device__ __forceinline__ void k64_row(
   const uint32_t v_off = vt64_lane_off(wave, lane);
 
   const int qpos = u * kBQ + wave * 32 + col;
-  const bool qvalid = qpos < N;
-  const int qrow = qvalid ? perm[qpos] : 0;
+  const int qtok = perm[qpos];  // -1 at a padding position
+  const bool qvalid = qtok >= 0;
+  const int qrow = qvalid ? qtok : 0;
   bf16x8 qf[G::QK_STEPS];
   {
     const uint4* src = (const uint4*)(q + head_off + (size_t)qrow * D);
@@ -1007,8 +1013,15 @@ __device__ __forceinline__ void k64_row(
   }
   const int count = SPARSE ? end - beg : NB;
   if constexpr (SPARSE) {
+    // a valid entry is staged with its block's token count in the high half
+    // (the tokens fill the block's first positions), an invalid one as -1
     const int32_t* colp = cols + (size_t)r * NB + beg;
-    for (int j = t; j < count; j += kThreads) smemCols[j] = colp[j];
+    for (int j = t; j < count; j += kThreads) {
+      const int c = colp[j];
+      int e = -1;
+      if (c >= 0 && c < NB) e = c | ((bcount ? bcount[c] : min(kBK, N - c * kBK)) << 16);
+      smemCols[j] = e;
+    }
   }
   wait_vm<0>();
   lds_barrier();
@@ -1018,21 +1031,37 @@ __device__ __forceinline__ void k64_row(
   const uint32_t vbase = col * kKT * 2 + ((half ^ swz<8>(col)) << 4);
 
   // Tile i of the row: block list[i / 2], keys [64 (i % 2), +64) of it; a
-  // list entry outside [0, NB) and a half past the last token are skipped.
-  // Returns the tile's packed (block, half) as 2 block + half, or -1 past the end.
+  // list entry outside [0, NB) and a half holding no token are skipped.
+  // Returns the tile as (2 block + half) | (its keys holding a token) << 16,
+  // or -1 past the end.
   auto next_valid = [&](int i, int* pos) -> int {
     for (; i < 2 * count; ++i) {
-      const int c = SPARSE ? smemCols[i >> 1] : (i >> 1);
-      if (c >= 0 && c < NB && c * kBK + (i & 1) * kKT < N) {
+      int c, n;
+      if constexpr (SPARSE) {
+        const int e = smemCols[i >> 1];
+        c = e & 0xFFFF;
+        n = e >> 16;  // -1 for an invalid entry
+      } else {
+        c = i >> 1;
+        n = min(kBK, N - c * kBK);
+      }
+      const int nv = n - (i & 1) * kKT;
+      if (nv > 0) {
         *pos = i;
-        return __builtin_amdgcn_readfirstlane(2 * c + (i & 1));
+        return __builtin_amdgcn_readfirstlane((2 * c + (i & 1)) | (min(nv, kKT) << 16));
       }
     }
     *pos = 2 * count;
     return -1;
   };
-  auto k_src = [&](int bt) { return Kb + (bt >> 1) * kBlockBytes + (bt & 1) * KT_BYTES; };
-  auto v_src = [&](int bt) { return Vb + (bt >> 1) * kBlockBytes + (bt & 1) * (kKT * 2); };
+  auto k_src = [&](int bt) {
+    bt &= 0xFFFF;
+    return Kb + (bt >> 1) * kBlockBytes + (bt & 1) * KT_BYTES;
+  };
+  auto v_src = [&](int bt) {
+    bt &= 0xFFFF;
+    return Vb + (bt >> 1) * kBlockBytes + (bt & 1) * (kKT * 2);
+  };
   auto issue_k = [&](int bt) { issue_steps<STEPS>(k_lds, k_src(bt), k_off); };
   auto issue_v = [&](int bt) { issue_steps_strided<STEPS, 32 * 256>(v_lds, v_src(bt), v_off); };
 
@@ -1071,7 +1100,7 @@ __device__ __forceinline__ void k64_row(
       }
       lds_barrier();  // every wave is done with the K tile
       if (has_next) issue_k(bt_nxt);
-      const int nv = N - (bt_cur >> 1) * kBK - (bt_cur & 1) * kKT;  // valid keys in this tile (> 0)
+      const int nv = bt_cur >> 16;  // keys of this tile holding a token (the first nv, > 0)
       if (nv < kKT) {
         const int base = 8 * half - nv;
         const uint32_t neg = __float_as_uint(-1.0e30f);
@@ -1200,9 +1229,9 @@ template <int D, bool SPARSE, bool LSE>
 __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ ktile, const uint16_t* __restrict__ vtile,
     uint16_t* __restrict__ o, float* __restrict__ lse, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ cols, const int4* __restrict__ units, const int32_t* __restrict__ unit_hdr,
-    bool ordered, int N, int n_pad, int NB, int rows, float scale_log2, int32_t* __restrict__ ctr,
-    float* __restrict__ part, float* __restrict__ pstats) {
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ bcount, const int4* __restrict__ units,
+    const int32_t* __restrict__ unit_hdr, bool ordered, int N, int n_pad, int NB, int rows, float scale_log2,
+    int32_t* __restrict__ ctr, float* __restrict__ part, float* __restrict__ pstats) {
   constexpr int KT_BYTES = kKT * D * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t smemK[KT_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t smemV[KT_BYTES];
@@ -1227,10 +1256,10 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
         continue;
       }
       k64_row<D, true, LSE>(un.x, un.y, un.z, un.w, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cols,
-                            N, n_pad, NB, scale_log2, part, pstats);
+                            bcount, N, n_pad, NB, scale_log2, part, pstats);
     } else {
-      k64_row<D, false, LSE>(w, 0, NB, -1, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cols, N, n_pad,
-                             NB, scale_log2, part, pstats);
+      k64_row<D, false, LSE>(w, 0, NB, -1, smemK, smemV, smemCols, q, ktile, vtile, o, lse, perm, cols, bcount,
+                             N, n_pad, NB, scale_log2, part, pstats);
     }
   }
 }
@@ -1238,7 +1267,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // Work units of a block-sparse call (one workgroup of 1024 threads).  The row
 // lists are walked in the caller's order (or row order); with T the total
 // list length and G the attention grid, L = max(kSplitMin, ceil(T / (G
-// kSplitPerWG))), doubled until the pieces fit the plan's partial slots, and a
+// kSplitPerWG))), doubled until the pieces fit the workspace's partial slots, and a
 // row of c > L entries becomes ceil(c / L) units of near-equal length, each
 // writing a partial slot, so that no unit holds more than about
 // 1 / kSplitPerWG of a workgroup's share of the work and the rows the call
@@ -1248,10 +1277,10 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // call).  Writes units[U] = {row, list begin, list end, slot or -1},
 // splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L}.  A split row
 // has c / L < pieces < 2 c / L, so P <= T / L <= G kSplitPerWG and
-// U <= rows + G kSplitPerWG: the plan sizes its tables by these bounds
+// U <= rows + G kSplitPerWG: the call's workspace holds tables of these bounds
 // (entries past a capacity are never written).
 constexpr int kSplitPerWG = 16;
-constexpr long long kSplitSlotBytes = 256ll << 20;  // partial workspace of a plan
+constexpr long long kSplitSlotBytes = 256ll << 20;  // partial results in a call's workspace
 constexpr int kSplitMin = 48;
 
 __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restrict__ cnt,
@@ -1367,8 +1396,8 @@ __global__ __launch_bounds__(256) void merge_split_rows_kernel(const int4* __res
     const int4 e = splits[sp];
     const int r = e.x, slot0 = e.y, pieces = e.z;
     const int bh = r / NB, u = r - bh * NB;
-    const int qpos = u * kBQ + qi;
-    if (qpos >= N) continue;
+    const int qtok = perm[u * kBQ + qi];  // -1 at a padding position
+    if (qtok < 0) continue;
     float m = -INFINITY;
     for (int p = 0; p < pieces; ++p) {
       const float* ps = pstats + (size_t)(slot0 + p) * 3 * kBQ;
@@ -1395,7 +1424,7 @@ __global__ __launch_bounds__(256) void merge_split_rows_kernel(const int4* __res
         acc[4 * j + 3] += w * x.w;
       }
     }
-    const size_t tok = (size_t)bh * N + perm[qpos];
+    const size_t tok = (size_t)bh * N + qtok;
     const float inv = lr > 0.f ? 1.f / lr : 0.f;
     uint2* dst = (uint2*)(o + tok * D + hd * HD);
 #pragma unroll
@@ -1445,8 +1474,9 @@ void launch_k64_lse(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE, LSE>), dim3(grid), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cols,
-                     (const int4*)p.d_units, p.d_unit_hdr, a.order != nullptr, p.S, p.n_pad, p.NB, p.rows,
-                     scale_log2, p.d_row_ctr, p.d_part, p.d_pstats);
+                     p.cfg.block_layout == TRA_BLOCKS_TILES ? p.d_bcount : nullptr, (const int4*)p.d_units,
+                     p.d_unit_hdr, a.order != nullptr, p.S, p.n_pad, p.NB, p.rows, scale_log2, p.d_row_ctr,
+                     p.d_part, p.d_pstats);
   if (SPARSE)
     hipLaunchKernelGGL((merge_split_rows_kernel<D, LSE>), dim3(std::max(1, std::min(p.splits_cap, 1024))),
                        dim3(256), 0, s, (const int4*)p.d_splits, p.d_unit_hdr, p.d_part, p.d_pstats,

@@ -79,8 +79,10 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
   const int bh = row / NB, u = row - bh * NB;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int q0 = u * B;
+  // a block's tokens fill its first n_video + n_text positions
+  const int n_u = binfo[(size_t)u * kBlockInfo + 6];
 
-  if (min(S, q0 + B) > N) {
+  if (binfo[(size_t)u * kBlockInfo + 9] > 0) {
     // a text block's row keeps every key block
     for (int v = t; v < NB; v += blockDim.x) {
       if (mask) mask[(size_t)row * NB + v] = 1;
@@ -89,7 +91,6 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
     if (t == 0) cnt[row] = NB;
     return;
   }
-  const int n_u = min(B, N - q0);
   const int u_frames = binfo[(size_t)u * kBlockInfo + 1] - binfo[(size_t)u * kBlockInfo + 0] + 1;
 
   for (int qi = t; qi < B; qi += blockDim.x) {
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(256) void block_mask_kernel(
     bool keep;
     if (v == u) {
       keep = true;  // every query keeps its own key, so the diagonal block is never empty
-    } else if (min(S, (v + 1) * B) > N) {
+    } else if (binfo[(size_t)v * kBlockInfo + 9] > 0) {
       keep = true;  // text keys stay visible
     } else {
       const int32_t* bi = binfo + (size_t)v * kBlockInfo;

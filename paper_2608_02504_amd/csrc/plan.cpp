@@ -15,7 +15,11 @@
 //    execution": a bounding-box test rejects pairs with no valid
 //    interaction);
 //  * text tokens of joint text-video attention (Sec. 3.2) follow the video
-//    tokens in the sequence and keep their order.
+//    tokens in the sequence and keep their order;
+//  * block layouts: packed (block u = positions [u b, (u+1) b) of the order)
+//    or tile-aligned padded blocks (one tile of one frame per block, a clipped
+//    edge tile padded; App. D's in-block redundancy is smallest when a block's
+//    spatial footprint is).
 #include <algorithm>
 #include <cmath>
 
@@ -41,11 +45,20 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   if (c.head_dim != 64 && c.head_dim != 128) { *why = "head_dim must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
   if (c.block != 64 && c.block != 128) { *why = "block must be 64 or 128"; return TRA_ERR_UNSUPPORTED; }
   if (c.dtype == TRA_BF16 && c.block != 128) { *why = "bf16 needs block 128"; return TRA_ERR_UNSUPPORTED; }
+  if (c.block_layout != TRA_BLOCKS_PACKED && c.block_layout != TRA_BLOCKS_TILES) { *why = "unknown block layout"; return TRA_ERR_INVALID_ARG; }
+  if (c.block_layout == TRA_BLOCKS_TILES) {
+    if ((int64_t)c.tile_h * c.tile_w != c.block) { *why = "tile-aligned blocks need tile_h * tile_w == block"; return TRA_ERR_INVALID_ARG; }
+    if (c.dtype != TRA_BF16) { *why = "tile-aligned blocks are supported on bf16 plans only"; return TRA_ERR_UNSUPPORTED; }
+  }
   const int64_t n = (int64_t)c.frames * c.height * c.width + c.text_tokens;
-  const int64_t nb = (n + c.block - 1) / c.block;
+  const int64_t nb = c.block_layout == TRA_BLOCKS_TILES
+                         ? (int64_t)c.frames * ((c.height + c.tile_h - 1) / c.tile_h) *
+                                   ((c.width + c.tile_w - 1) / c.tile_w) +
+                               (c.text_tokens + c.block - 1) / c.block
+                         : (n + c.block - 1) / c.block;
   if (nb > kMaxBlocks) { *why = "more than 4096 blocks per head"; return TRA_ERR_UNSUPPORTED; }
   const int64_t rows = (int64_t)c.batch * c.heads * nb;
-  if (rows * nb >= (int64_t)1 << 31 || (int64_t)c.batch * c.heads * n >= (int64_t)1 << 31) {
+  if (rows * nb >= (int64_t)1 << 31 || (int64_t)c.batch * c.heads * nb * c.block >= (int64_t)1 << 31) {
     *why = "batch * heads * tokens too large for 32-bit indexing";
     return TRA_ERR_UNSUPPORTED;
   }
@@ -68,9 +81,12 @@ double normal_quantile(double p) {
 void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
                        bool with_thr, bool with_thr1, bool with_blocks, bool with_kinfo) {
   const int F = c.frames, H = c.height, W = c.width, b = c.block;
+  const bool tiles = c.block_layout == TRA_BLOCKS_TILES;
   t->N = F * H * W;
   t->S = t->N + c.text_tokens;
-  t->NB = (t->S + b - 1) / b;
+  const int tiles_h = (H + c.tile_h - 1) / c.tile_h, tiles_w = (W + c.tile_w - 1) / c.tile_w;
+  t->NB = tiles ? F * tiles_h * tiles_w + (c.text_tokens + b - 1) / b : (t->S + b - 1) / b;
+  t->P = tiles ? t->NB * b : t->S;
   t->n_cap = (H - 1) * (H - 1) + (W - 1) * (W - 1);
 
   std::vector<int32_t> perm;
@@ -82,16 +98,34 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
       for (int tx = 0; tx < W; tx += c.tile_w)
         for (int x = ty; x < std::min(H, ty + c.tile_h); ++x)
           for (int y = tx; y < std::min(W, tx + c.tile_w); ++y) frame.push_back(x * W + y);
-    perm.resize(t->S);
+    std::vector<int32_t> packed(t->S);
     for (int f = 0; f < F; ++f)
-      for (int p = 0; p < H * W; ++p) perm[(size_t)f * H * W + p] = f * H * W + frame[p];
-    for (int p = t->N; p < t->S; ++p) perm[p] = p;
+      for (int p = 0; p < H * W; ++p) packed[(size_t)f * H * W + p] = f * H * W + frame[p];
+    for (int p = t->N; p < t->S; ++p) packed[p] = p;
+    if (tiles) {
+      // one block per tile: the tile's tokens (row-major) then padding
+      perm.assign((size_t)t->P, -1);
+      size_t at = 0;
+      for (int f = 0; f < F; ++f)
+        for (int ty = 0; ty < H; ty += c.tile_h)
+          for (int tx = 0; tx < W; tx += c.tile_w) {
+            size_t j = at;
+            for (int x = ty; x < std::min(H, ty + c.tile_h); ++x)
+              for (int y = tx; y < std::min(W, tx + c.tile_w); ++y) perm[j++] = (f * H + x) * W + y;
+            at += b;
+          }
+      for (int s0 = 0; s0 < c.text_tokens; s0 += b, at += b)
+        for (int j = 0; j < b && s0 + j < c.text_tokens; ++j) perm[at + j] = t->N + s0 + j;
+      if (with_perm_coord) t->perm_attn = std::move(packed);
+    } else {
+      perm = std::move(packed);
+    }
   }
   if (with_perm_coord) {
-    t->coord.assign(t->S, 0);
-    for (int p = 0; p < t->N; ++p) {
+    t->coord.assign(t->P, 0);
+    for (int p = 0; p < t->P; ++p) {
       const int i = perm[p];
-      t->coord[p] = pack_coord(i / (H * W), (i / W) % H, i % W);
+      if (i >= 0 && i < t->N) t->coord[p] = pack_coord(i / (H * W), (i / W) % H, i % W);
     }
   }
   if (with_thr) {
@@ -114,13 +148,21 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
       }
   }
   if (with_blocks) {
+    // Every block's tokens fill its first positions: video tokens first, then
+    // text tokens (only the packed layout mixes the two, in one block).
     t->blocks.assign((size_t)t->NB * kBlockInfo, 0);
     for (int u = 0; u < t->NB; ++u) {
       int fmin = F, fmax = -1, xmin = H, xmax = -1, ymin = W, ymax = -1;
-      int rmin = t->N, rmax = -1;
-      const int lo = u * b, hi_all = std::min(t->S, lo + b), hi = std::min(t->N, hi_all);
+      int rmin = t->N, rmax = -1, n_video = 0, n_text = 0;
+      const int lo = u * b, hi = std::min(t->P, lo + b);
       for (int p = lo; p < hi; ++p) {
         const int i = perm[p];
+        if (i < 0) continue;
+        if (i >= t->N) {
+          ++n_text;
+          continue;
+        }
+        ++n_video;
         const int f = i / (H * W), x = (i / W) % H, y = i % W;
         fmin = std::min(fmin, f); fmax = std::max(fmax, f);
         xmin = std::min(xmin, x); xmax = std::max(xmax, x);
@@ -129,8 +171,7 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
       }
       int32_t* o = &t->blocks[(size_t)u * kBlockInfo];
       o[0] = fmin; o[1] = fmax; o[2] = xmin; o[3] = xmax; o[4] = ymin; o[5] = ymax;
-      o[6] = std::max(0, hi - lo); o[7] = rmin; o[8] = rmax;
-      o[9] = hi_all - std::max(lo, t->N) > 0 ? hi_all - std::max(lo, t->N) : 0;
+      o[6] = n_video; o[7] = rmin; o[8] = rmax; o[9] = n_text;
     }
   }
   if (with_kinfo) {
@@ -138,21 +179,23 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
     // zero block after the last, so a 1 KB copy of the last block stays in
     // bounds).  2-D: x | y << 16, 1-D: the raster index; plus a flag bit
     // (bit 15 for 2-D, bit 30 for 1-D) when the key lies in the block's second
-    // frame (a block of at most H*W tokens spans at most two), and bit 31 for
-    // a text key.  Positions past S stay 0 (the ragged tail is masked apart).
+    // frame (a packed block of at most H*W tokens spans at most two; a tile
+    // block one), and bit 31 for a text key.  Padding stays 0 (masked apart by
+    // the block's token count).
     const bool one_d = c.distance == TRA_DIST_1D;
     t->kinfo.assign((size_t)(t->NB + 1) * kKeyInfo, 0);
     for (int u = 0; u < t->NB; ++u) {
-      const int f0 = u * b < t->N ? perm[(size_t)u * b] / (H * W) : 0;
+      const int first = u * b < t->P ? perm[(size_t)u * b] : -1;
+      const int f0 = first >= 0 && first < t->N ? first / (H * W) : 0;
       for (int j = 0; j < b; ++j) {
         const int p = u * b + j;
+        const int i = p < t->P ? perm[p] : -1;
         uint32_t word = 0;
-        if (p < t->N) {
-          const int i = perm[p];
+        if (i >= 0 && i < t->N) {
           const bool second = i / (H * W) != f0;
           word = one_d ? (uint32_t)i | (second ? 1u << 30 : 0u)
                        : (uint32_t)((i / W) % H) | ((uint32_t)(i % W) << 16) | (second ? 1u << 15 : 0u);
-        } else if (p < t->S) {
+        } else if (i >= t->N) {
           word = 1u << 31;
         }
         t->kinfo[(size_t)u * kKeyInfo + j] = (int32_t)word;

@@ -30,9 +30,11 @@ constexpr int kRowCounters = 128;  // ints of the attention row-queue counters
 
 // Host-side tables of one shape (plan.cpp).
 struct HostTables {
-  int32_t N = 0, S = 0, NB = 0, n_cap = 0;  // video tokens, all tokens, blocks over S
-  std::vector<int32_t> perm;    // [S] tile-major position -> token index (text: N + t)
-  std::vector<int32_t> coord;   // [S] packed (f, x, y) of a video position, 0 for text
+  int32_t N = 0, S = 0, NB = 0, n_cap = 0;  // video tokens, all tokens, blocks of the layout
+  int32_t P = 0;                // positions of the block layout's order (S packed, NB * b tiles)
+  std::vector<int32_t> perm;    // [P] position -> token index (text: N + t), -1 = padding
+  std::vector<int32_t> perm_attn;  // tile-aligned layout only: the packed order [S]
+  std::vector<int32_t> coord;   // [P] packed (f, x, y) of a video position, 0 otherwise
   std::vector<int32_t> thr;     // [(n_cap + 1) * F] 2-D squared thresholds
   std::vector<int32_t> thr1;    // [(n_cap + 1) * F] 1-D thresholds
   std::vector<int32_t> blocks;  // [NB * kBlockInfo]
@@ -54,10 +56,21 @@ struct tra_plan_s {
   int device = 0;
   int32_t N = 0;   // video tokens F*H*W
   int32_t S = 0;   // all tokens (video then text): the row length of every tensor
+  // Block layout (mask, block-sparse and token-level calls): NB blocks per
+  // head, rows = batch * heads * NB query-block rows, n_pad = NB * block
+  // positions; d_perm [n_pad]: position -> token, -1 at padding (the packed
+  // layout's positions past S, a clipped tile's tail); d_coord [n_pad];
+  // d_bcount [NB]: tokens of each block (they fill its first positions).
   int32_t NB = 0, n_cap = 0, rows = 0;
   double z_tau = 0.0;  // Phi^{-1}(tau), lognormal budget mapping
   int32_t* d_perm = nullptr;
   int32_t* d_coord = nullptr;
+  int32_t* d_bcount = nullptr;
+  // Layout of the calls defined over tokens (entropy, dense): always the
+  // packed order.  Equal to the block layout's fields for packed plans (the
+  // same device table); for tile-aligned plans a table of its own.
+  int32_t NBa = 0, rowsa = 0, n_pada = 0;
+  int32_t* d_perma = nullptr;
   int32_t* d_thr = nullptr;
   int32_t* d_thr1 = nullptr;  // 1-D thresholds (TRA_DIST_1D plans only)
   int32_t* d_blocks = nullptr;

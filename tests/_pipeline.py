@@ -43,10 +43,12 @@ class Run:
     """All stage outputs of one pass of the path on the GPU."""
 
     def __init__(self, w, rule="vote", with_order=True, inputs=None, radius_override=None,
-                 budget="uniform", distance="2d", entropy_override=None):
+                 budget="uniform", distance="2d", entropy_override=None, block_layout="packed"):
         import torch
         self.w = w
-        self.cfg = tra.Config.from_workload(w, rule=rule, budget=budget, distance=distance)
+        self.radius_override = radius_override
+        self.cfg = tra.Config.from_workload(w, rule=rule, budget=budget, distance=distance,
+                                            block_layout=block_layout)
         self.plan = tra.Plan(self.cfg)
         log(f"workload {w.name} S={w.n_tokens} (text {w.text_tokens}) heads={w.heads} d={w.head_dim} "
             f"{w.dtype} rule={rule} budget={budget} distance={distance}")
@@ -98,10 +100,12 @@ class Run:
         return t.cpu().numpy()
 
 
-def sample_blocks(w, n_blocks_per_head: int, seed: int):
-    """Seeded query blocks per (batch, head); always includes the ragged last block."""
+def sample_blocks(w, n_blocks_per_head: int, seed: int, nb=None):
+    """Seeded query blocks per (batch, head); always includes the last block
+    (the ragged one of a packed layout).  nb: blocks per head (default the
+    packed layout's)."""
     rng = np.random.default_rng(seed)
-    nb = w.n_blocks
+    nb = w.n_blocks if nb is None else nb
     out = {}
     for b in range(w.batch):
         for h in range(w.heads):
@@ -115,13 +119,19 @@ def sample_blocks(w, n_blocks_per_head: int, seed: int):
 
 
 class OracleTables:
-    def __init__(self, w):
+    def __init__(self, w, block_layout="packed"):
         self.F, self.H, self.W = w.frames, w.height, w.width
         self.ncap = O.n_cap(w.height, w.width)
         self.thr = O.threshold_table(self.ncap, w.frames, w.gamma)
         self.disk = O.disk_count_table(w.height, w.width, self.ncap)
-        self.perm = O.joint_order(O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w),
-                                  w.text_tokens)
+        if block_layout == "tiles":
+            self.perm = O.tile_aligned_order(w.frames, w.height, w.width, w.tile_h, w.tile_w, w.block,
+                                             text_tokens=w.text_tokens)
+        else:
+            self.perm = O.joint_order(O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w),
+                                      w.text_tokens)
+        self.n_blocks = -(-len(self.perm) // w.block)
+        self.sizes = O.block_sizes(self.perm, w.block)
         self.f, self.x, self.y = O.grid_coords(w.frames, w.height, w.width)
 
 
@@ -155,7 +165,7 @@ def check_head(run: Run, tabs: OracleTables, b: int, h: int, blocks, tol_o: floa
     q = synth.to_f64(run.q_np[b, h], w.dtype)
     k = synth.to_f64(run.k_np[b, h], w.dtype)
     v = synth.to_f64(run.v_np[b, h], w.dtype)
-    rows = np.concatenate([perm[u * bs:min((u + 1) * bs, N)] for u in blocks])
+    rows = np.concatenate([O.block_tokens(perm, bs, u) for u in blocks])
 
     O_ref = lse_ref = None
     if dense:
@@ -210,13 +220,17 @@ def check_head(run: Run, tabs: OracleTables, b: int, h: int, blocks, tol_o: floa
     assert np.array_equal(khv[~near], khat_ref[~near]), "budget mismatch"
     assert (np.abs(khv[near] - khat_ref[near]) <= 1).all(), "budget mismatch at an integer boundary"
     fv, xv, yv = tabs.f[rv], tabs.x[rv], tabs.y[rv]
-    n_ref = O.select_radius(khat_ref, fv, xv, yv, tabs.F, tabs.thr, tabs.disk)
     nv_gpu = n_gpu[video]
-    assert np.array_equal(nv_gpu[~near], n_ref[~near]), \
-        f"radius mismatch at {np.nonzero((nv_gpu != n_ref) & ~near)[0][:5]}"
-    if near.any():
-        n_alt = O.select_radius(khv[near], fv[near], xv[near], yv[near], tabs.F, tabs.thr, tabs.disk)
-        assert np.array_equal(nv_gpu[near], n_alt), "radius mismatch at an integer budget boundary"
+    if run.radius_override is not None:
+        # the radii the test wrote over the budget stage's output
+        assert (nv_gpu == int(run.radius_override)).all(), "forced radius"
+    else:
+        n_ref = O.select_radius(khat_ref, fv, xv, yv, tabs.F, tabs.thr, tabs.disk)
+        assert np.array_equal(nv_gpu[~near], n_ref[~near]), \
+            f"radius mismatch at {np.nonzero((nv_gpu != n_ref) & ~near)[0][:5]}"
+        if near.any():
+            n_alt = O.select_radius(khv[near], fv[near], xv[near], yv[near], tabs.F, tabs.thr, tabs.disk)
+            assert np.array_equal(nv_gpu[near], n_alt), "radius mismatch at an integer budget boundary"
 
     # block mask rows (Alg. 1) from the GPU radii: bit-exact
     n_full = run.rad[b, h].cpu().numpy()
@@ -275,5 +289,6 @@ def check_lists(run: Run):
     assert mask[:, :, idx, idx].all()
 
 
-def retained_fraction(run: Run):
-    return O.retained_fraction(run.mask.cpu().numpy().astype(bool), run.w.n_tokens, run.w.block)
+def retained_fraction(run: Run, tabs=None):
+    sizes = tabs.sizes if tabs is not None else None
+    return O.retained_fraction(run.mask.cpu().numpy().astype(bool), run.w.n_tokens, run.w.block, sizes=sizes)

@@ -54,9 +54,36 @@ def test_host_tables_match_oracle(name):
         assert list(blocks[u]) == want, u
 
 
+@pytest.mark.parametrize("name", ["wan13b_480p", "wan14b_720p", "hunyuan_joint_720p", "ragged_text"])
+def test_tile_aligned_host_tables_match_oracle(name):
+    """Tile-aligned padded blocks: the plan's order equals the oracle's padded
+    order (-1 at padding), and every block's info is that of its own tokens."""
+    w = (synth.Workload("ragged_text", 1, 2, 128, "bf16", 3, 11, 29, 128, 0.25, 4.0, 0.6,
+                        tile_h=8, tile_w=16, text_tokens=130) if name == "ragged_text" else synth.workload(name))
+    cfg = tra.Config.from_workload(w, block_layout="tiles")
+    perm, thr, thr1, blocks, ncap = tra.tra_plan_host_tables(cfg)
+    want = O.tile_aligned_order(w.frames, w.height, w.width, w.tile_h, w.tile_w, w.block,
+                                text_tokens=w.text_tokens)
+    assert np.array_equal(perm, want)
+    assert cfg.n_blocks == len(want) // w.block == blocks.shape[0]
+    N = w.n_video
+    f, x, y = O.grid_coords(w.frames, w.height, w.width)
+    for u in range(cfg.n_blocks):
+        r = O.block_tokens(want, w.block, u)
+        rv, n_text = r[r < N], int((r >= N).sum())
+        if len(rv):
+            exp = [f[rv].min(), f[rv].max(), x[rv].min(), x[rv].max(), y[rv].min(), y[rv].max(),
+                   len(rv), rv.min(), rv.max(), n_text]
+        else:
+            exp = [w.frames, -1, w.height, -1, w.width, -1, 0, N, -1, n_text]
+        assert list(blocks[u]) == exp, u
+
+
 def test_tiny_layout_sizes():
     cfg = tra.Config.from_workload(synth.workload("wan14b_720p"))
     assert cfg.n_tokens == 75600 and cfg.n_blocks == 591
+    cfg_t = tra.Config.from_workload(synth.workload("wan14b_720p"), block_layout="tiles")
+    assert cfg_t.n_blocks == 21 * 6 * 5 == 630 and cfg_t.n_positions == 630 * 128
     cfg3 = tra.Config.from_workload(synth.workload("hunyuan_720p"))
     assert cfg3.n_tokens == 118800 and cfg3.n_blocks == 929
     assert cfg3.n_tokens - (cfg3.n_blocks - 1) * 128 == 16
@@ -72,6 +99,9 @@ def test_tiny_layout_sizes():
     (dict(rule="maj"), 1), (dict(batch=0), 1), (dict(budget="gamma"), 1),
     (dict(distance="3d"), 1), (dict(text_tokens=-1), 1),
     (dict(text_tokens=4096 * 128), 2),   # more than 4096 blocks
+    (dict(block_layout="tiles", tile_h=8, tile_w=8), 1),           # a tile must hold one block
+    (dict(block_layout="tiles", dtype="fp32", block=64, tile_h=8, tile_w=8), 2),  # bf16 only
+    (dict(block_layout="diag"), 1),
 ])
 def test_invalid_configs_rejected(change, status):
     base = dict(batch=1, heads=2, frames=3, height=8, width=16, head_dim=128)
