@@ -113,6 +113,50 @@ int main() {
       }
     }
   }
+  // tile-aligned padded blocks: NB * b positions, every token once, tokens a
+  // prefix of each block, each video block inside one tile of one frame
+  {
+    const std::vector<tra_config> tiled = {
+        make(4, 13, 37, 128, 128, 8, 16, 77, TRA_BF16, TRA_DIST_2D),
+        make(7, 5, 9, 64, 128, 8, 16, 0, TRA_BF16, TRA_DIST_1D),
+        make(21, 45, 80, 128, 128, 8, 16, 0, TRA_BF16, TRA_DIST_2D)};
+    for (size_t ci = 0; ci < tiled.size(); ++ci) {
+      tra_config c = tiled[ci];
+      c.block_layout = TRA_BLOCKS_TILES;
+      const int ic = 300 + (int)ci;
+      std::string why;
+      expect(tra::validate_config(&c, &why) == TRA_OK, "valid tiled config rejected", ic);
+      tra::HostTables t;
+      tra::build_host_tables(c, &t, true, true, false, true, true);
+      const int N = c.frames * c.height * c.width, S = N + c.text_tokens, b = c.block;
+      const int tiles = c.frames * ((c.height + c.tile_h - 1) / c.tile_h) * ((c.width + c.tile_w - 1) / c.tile_w);
+      expect(t.NB == tiles + (c.text_tokens + b - 1) / b && t.P == t.NB * b && (int)t.perm.size() == t.P,
+             "tiled sizes", ic);
+      expect((int)t.perm_attn.size() == S, "packed order of the token calls", ic);
+      std::vector<int> seen(S, 0);
+      for (int u = 0; u < t.NB; ++u) {
+        const int32_t* bi = &t.blocks[(size_t)u * tra::kBlockInfo];
+        const int n = bi[6] + bi[9];
+        for (int j = 0; j < b; ++j) {
+          const int i = t.perm[(size_t)u * b + j];
+          if ((j < n) != (i >= 0)) { expect(false, "tokens not a prefix of the block", ic); break; }
+          if (i < 0) continue;
+          if (i >= S) { expect(false, "tiled perm out of range", ic); break; }
+          ++seen[i];
+          if (i < N) {
+            const int f = i / (c.height * c.width), x = (i / c.width) % c.height, y = i % c.width;
+            if (f != bi[0] || f != bi[1] || x / c.tile_h != bi[2] / c.tile_h || y / c.tile_w != bi[4] / c.tile_w ||
+                x < bi[2] || x > bi[3] || y < bi[4] || y > bi[5]) {
+              expect(false, "tiled block not one tile of one frame", ic);
+              break;
+            }
+          }
+        }
+      }
+      for (int i = 0; i < S; ++i)
+        if (seen[i] != 1) { expect(false, "tiled perm not a bijection", ic); break; }
+    }
+  }
   // invalid configurations are rejected before any table is built
   std::vector<tra_config> bad;
   tra_config b0 = good[1]; b0.head_dim = 96; bad.push_back(b0);
@@ -123,6 +167,8 @@ int main() {
   tra_config b5 = good[1]; b5.tau = 1.0f; bad.push_back(b5);
   tra_config b6 = good[1]; b6.text_tokens = -1; bad.push_back(b6);
   tra_config b7 = good[1]; b7.distance = 7; bad.push_back(b7);
+  tra_config b8 = good[1]; b8.block_layout = TRA_BLOCKS_TILES; b8.tile_w = 8; bad.push_back(b8);
+  tra_config b9 = good[0]; b9.block_layout = TRA_BLOCKS_TILES; bad.push_back(b9);  // fp32
   for (size_t i = 0; i < bad.size(); ++i) {
     std::string why;
     expect(tra::validate_config(&bad[i], &why) != TRA_OK && !why.empty(), "invalid config accepted",
