@@ -98,7 +98,7 @@ WsLayout ws_layout(const tra_plan_s& p, int call) {
     if (call == TRA_CALL_SPARSE) {
       L.units = take((size_t)p.units_cap * 4 * sizeof(int32_t));
       L.splits = take((size_t)p.splits_cap * 4 * sizeof(int32_t));
-      L.hdr = take(4 * sizeof(int32_t));
+      L.hdr = take(tra::kUnitHdrInts * sizeof(int32_t));
       L.part = take((size_t)p.slots_cap * 128 * p.cfg.head_dim * sizeof(float));
       L.pstats = take((size_t)p.slots_cap * 3 * 128 * sizeof(float));
     }
@@ -267,7 +267,7 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
         return fail(TRA_ERR_ALLOC, std::string("plan key-info table: ") + hipGetErrorString(e));
       }
       p->split_wg_cap = tra::k64_sparse_grid_cap(*p);
-      tra::split_capacities(p->split_wg_cap, p->rows, cfg->head_dim, &p->units_cap, &p->splits_cap,
+      tra::split_capacities(p->split_wg_cap, p->rows, p->NB, cfg->head_dim, &p->units_cap, &p->splits_cap,
                            &p->slots_cap);
     }
     // the no-allocation entry point's scratch array on this device: its

@@ -1202,17 +1202,18 @@ __device__ __forceinline__ void k64_row(
 
 // Queue of work units (thread 0 of a workgroup only): with `single`, one
 // counter walks the units in table order (the caller's row order); otherwise
-// per-XCD contiguous ranges with stealing, as next_row.  Returns -1 once all
-// is drained.
-__device__ __forceinline__ int next_unit(int32_t* ctr, bool single, int n, int xcd, int& steal) {
+// XCD x drains its segment [seg[x], seg[x + 1]) of the table, then takes units
+// from the other segments in turn, as next_row.  Returns -1 once all is
+// drained.
+__device__ __forceinline__ int next_unit(int32_t* ctr, bool single, int n, const int32_t* __restrict__ seg, int xcd,
+                                         int& steal) {
   if (single) {
     const int k = atomicAdd(&ctr[0], 1);
     return k < n ? k : -1;
   }
-  const int per = n / 8, rem = n % 8;
   while (steal < 8) {
     const int qd = (xcd + steal) & 7;
-    const int beg = qd * per + min(qd, rem), cnt = per + (qd < rem ? 1 : 0);
+    const int beg = seg[qd], cnt = seg[qd + 1] - beg;
     const int k = atomicAdd(&ctr[qd * 16], 1);
     if (k < cnt) return beg + k;
     ++steal;
@@ -1242,7 +1243,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
   for (;;) {
     if (threadIdx.x == 0) {
       int steal = s_steal;
-      s_row = SPARSE ? next_unit(ctr, ordered, n_work, blockIdx.x & 7, steal)
+      s_row = SPARSE ? next_unit(ctr, ordered, n_work, unit_hdr + 4, blockIdx.x & 7, steal)
                      : next_row(ctr, nullptr, rows, blockIdx.x & 7, steal);
       s_steal = steal;
     }
@@ -1264,21 +1265,33 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
   }
 }
 
-// Work units of a block-sparse call (one workgroup of 1024 threads).  The row
-// lists are walked in the caller's order (or row order); with T the total
-// list length and G the attention grid, L = max(kSplitMin, ceil(T / (G
-// kSplitPerWG))), doubled until the pieces fit the workspace's partial slots, and a
-// row of c > L entries becomes ceil(c / L) units of near-equal length, each
-// writing a partial slot, so that no unit holds more than about
+// Work units of a block-sparse call (one workgroup of 1024 threads).  With T
+// the total list length and G the attention grid, L = max(kSplitMin, ceil(T /
+// (G kSplitPerWG))), doubled until the pieces fit the workspace's partial
+// slots, and a row of c > L entries becomes ceil(c / L) units of near-equal
+// length, each writing a partial slot, so that no unit holds more than about
 // 1 / kSplitPerWG of a workgroup's share of the work and the rows the call
 // waits on at its end are short, while short rows are never cut into pieces
 // whose fixed costs (query load, partial write, merge) would dominate.  Rows of
 // at most L entries are one unit each (and give the same result as an unsplit
-// call).  Writes units[U] = {row, list begin, list end, slot or -1},
-// splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L}.  A split row
-// has c / L < pieces < 2 c / L, so P <= T / L <= G kSplitPerWG and
-// U <= rows + G kSplitPerWG: the call's workspace holds tables of these bounds
-// (entries past a capacity are never written).
+// call).
+//
+// Unit order.  With the caller's row order, units follow it (a row's pieces
+// consecutive) and one counter walks them.  Otherwise the rows are cut into
+// eight contiguous segments, one per XCD queue (hdr[4 + x] .. hdr[5 + x]), and
+// inside a segment the pieces of its split rows come first, piece-major (piece
+// 0 of every split row, then piece 1, ...; a row with fewer pieces than the
+// segment's most leaves placeholder units), then its other rows in row order.
+// Long rows keep most of their lists alike (rows whose queries mostly have
+// the full radius keep every block), so the split pieces a queue's workgroups
+// run side by side walk the same key blocks, and the L2 serves them to all.
+//
+// Writes units[U] = {row, list begin, list end, slot or -1} (row -1: a
+// placeholder), splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L,
+// 0, segment starts x 9}.  A split row has c / L < pieces < 2 c / L, so P <= T
+// / L <= G kSplitPerWG; with the placeholders U <= rows + max(G kSplitPerWG,
+// ceil(NB / kSplitMin) slots / 2): the call's workspace holds tables of these
+// bounds (entries past a capacity are never written).
 constexpr int kSplitPerWG = 16;
 constexpr long long kSplitSlotBytes = 256ll << 20;  // partial results in a call's workspace
 constexpr int kSplitMin = 48;
@@ -1290,9 +1303,24 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
                                                           int slots_cap, int32_t* __restrict__ hdr) {
   __shared__ long long s_red[1024];
   __shared__ int s_scan[3][1024];
+  __shared__ int s_seg[4][1024];  // per thread, segmented: split rows, other rows, max pieces
+  __shared__ int s_base[9];
   const int t = threadIdx.x;
-  const int per = (rows + 1023) / 1024;
-  const int k0 = min(rows, t * per), k1 = min(rows, k0 + per);
+  const bool segmented = order == nullptr;
+  // this thread's positions [k0, k1) of the walk: in segment t / 128 for the
+  // per-XCD queues, else 1/1024 of the caller's order
+  int k0, k1;
+  if (segmented) {
+    const int x = t >> 7, ls = t & 127;
+    const int r0 = (int)((long long)rows * x / 8), r1 = (int)((long long)rows * (x + 1) / 8);
+    const int per = (r1 - r0 + 127) / 128;
+    k0 = min(r1, r0 + ls * per);
+    k1 = min(r1, k0 + per);
+  } else {
+    const int per = (rows + 1023) / 1024;
+    k0 = min(rows, t * per);
+    k1 = min(rows, k0 + per);
+  }
   auto row_at = [&](int k) { return order ? order[k] : k; };
   auto len_of = [&](int r) { return (r >= 0 && r < rows) ? min(max(cnt[r], 0), NB) : -1; };
   long long tot = 0;
@@ -1308,9 +1336,9 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
   int L = (int)max((long long)kSplitMin, (total + share - 1) / share);
   // per thread: units, slots and split rows of its positions; L doubles until
   // the pieces of the split rows fit the partial slots
-  int nu, ns, np;
+  int nu, ns, np, nw, pmx;
   for (;;) {
-    nu = ns = np = 0;
+    nu = ns = np = nw = pmx = 0;
     for (int k = k0; k < k1; ++k) {
       const int c = len_of(row_at(k));
       if (c < 0) continue;
@@ -1319,6 +1347,9 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
       if (pieces > 1) {
         ns += pieces;
         ++np;
+        pmx = max(pmx, pieces);
+      } else {
+        ++nw;
       }
     }
     __syncthreads();
@@ -1334,21 +1365,83 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
   s_scan[0][t] = nu;
   s_scan[1][t] = ns;
   s_scan[2][t] = np;
+  s_seg[0][t] = np;
+  s_seg[1][t] = nw;
+  s_seg[2][t] = pmx;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {  // inclusive scans
-    int a0 = 0, a1 = 0, a2 = 0;
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive scans; s_seg within 128-thread segments
+    int a0 = 0, a1 = 0, a2 = 0, g0 = 0, g1 = 0, g2 = 0;
     if (t >= off) {
       a0 = s_scan[0][t - off];
       a1 = s_scan[1][t - off];
       a2 = s_scan[2][t - off];
     }
+    if ((t & 127) >= off) {
+      g0 = s_seg[0][t - off];
+      g1 = s_seg[1][t - off];
+      g2 = s_seg[2][t - off];
+    }
     __syncthreads();
     s_scan[0][t] += a0;
     s_scan[1][t] += a1;
     s_scan[2][t] += a2;
+    s_seg[0][t] += g0;
+    s_seg[1][t] += g1;
+    s_seg[2][t] = max(s_seg[2][t], g2);
     __syncthreads();
   }
-  int ub = s_scan[0][t] - nu, sb = s_scan[1][t] - ns, pb = s_scan[2][t] - np;
+  // segment starts: segment x holds (its most pieces) x (its split rows)
+  // piece-major units, then its other rows
+  if (t == 0) {
+    int b = 0;
+    for (int x = 0; x < 8; ++x) {
+      s_base[x] = b;
+      const int last = x * 128 + 127;
+      b += segmented ? s_seg[2][last] * s_seg[0][last] + s_seg[1][last] : 0;
+    }
+    s_base[8] = b;
+  }
+  __syncthreads();
+  int sb = s_scan[1][t] - ns, pb = s_scan[2][t] - np;
+  if (segmented) {
+    const int x = t >> 7, last = x * 128 + 127;
+    const int n_split = s_seg[0][last], p_most = s_seg[2][last];
+    const int base = s_base[x];
+    int ks = s_seg[0][t] - np, kw = s_seg[1][t] - nw;  // ranks of this thread's first rows
+    for (int k = k0; k < k1; ++k) {
+      const int r = row_at(k);
+      const int c = len_of(r);
+      if (c < 0) continue;
+      const int pieces = c > L ? (c + L - 1) / L : 1;
+      if (pieces == 1) {
+        const int pos = base + p_most * n_split + kw;
+        if (pos < units_cap) units[pos] = make_int4(r, 0, c, -1);
+        ++kw;
+        continue;
+      }
+      const bool fits = sb + pieces <= slots_cap && pb < splits_cap;  // always, by the bounds above
+      for (int s = 0; s < p_most; ++s) {
+        int4 un = make_int4(-1, 0, 0, -1);
+        if (s < pieces && fits)
+          un = make_int4(r, (int)((long long)c * s / pieces), (int)((long long)c * (s + 1) / pieces), sb + s);
+        const int pos = base + s * n_split + ks;
+        if (pos < units_cap) units[pos] = un;
+      }
+      if (fits) splits[pb] = make_int4(r, sb, pieces, 0);
+      ++ks;
+      sb += pieces;
+      ++pb;
+    }
+    if (t == 1023) {
+      hdr[0] = min(s_base[8], units_cap);
+      hdr[1] = min(s_scan[2][1023], splits_cap);
+      hdr[2] = L;
+      hdr[3] = 0;
+      for (int i = 0; i < 9; ++i) hdr[4 + i] = min(s_base[i], units_cap);
+    }
+    return;
+  }
+  int ub = s_scan[0][t] - nu;
   for (int k = k0; k < k1; ++k) {
     const int r = row_at(k);
     const int c = len_of(r);
@@ -1374,6 +1467,7 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
     hdr[0] = min(s_scan[0][1023], units_cap);
     hdr[1] = min(s_scan[2][1023], splits_cap);
     hdr[2] = L;
+    hdr[3] = 0;
   }
 }
 
@@ -1778,12 +1872,16 @@ int k64_sparse_grid_cap(const tra_plan_s& p) {
   return p.cfg.head_dim == 64 ? k64_sparse_grid_cap_d<64>(p) : k64_sparse_grid_cap_d<128>(p);
 }
 
-void split_capacities(int grid_cap, int rows, int head_dim, int* units_cap, int* splits_cap, int* slots_cap) {
+void split_capacities(int grid_cap, int rows, int NB, int head_dim, int* units_cap, int* splits_cap,
+                      int* slots_cap) {
   const long long share = (long long)grid_cap * kSplitPerWG;
-  *units_cap = (int)std::min<long long>(INT_MAX, rows + share + 1);
-  *splits_cap = (int)std::min<long long>(INT_MAX, share + 1);
   const long long slot_bytes = (long long)kBQ * (head_dim + 3) * 4;
   *slots_cap = (int)std::min<long long>(2 * share + 1, kSplitSlotBytes / slot_bytes);
+  *splits_cap = (int)std::min<long long>(INT_MAX, share + 1);
+  // piece-major segments: at most ceil(NB / kSplitMin) units per split row,
+  // and at most slots / 2 split rows
+  const long long seg = (long long)((NB + kSplitMin - 1) / kSplitMin) * (*slots_cap / 2 + 1);
+  *units_cap = (int)std::min<long long>(INT_MAX, rows + std::max(share, seg) + 1);
 }
 
 hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {

@@ -98,7 +98,8 @@ struct tra_plan_s {
   int32_t n_cu = 0;
   // bf16 plans, call workspace: work units of block-sparse calls (rows cut into pieces of at
   // most L list entries) and the pieces' partial results: units [units_cap]
-  // int4, split rows [splits_cap] int4, header {units, split rows, L}, partial
+  // int4, split rows [splits_cap] int4, header {units, split rows, L, 0, nine
+  // segment starts of the per-XCD queues} (kUnitHdrInts ints), partial
   // outputs [slots_cap][128][d] fp32 and statistics [slots_cap][3][128] fp32
   // (running max, rounded and fp32 sums), for at most split_wg_cap workgroups;
   // the capacities are the plan's, fixed at creation.
@@ -133,7 +134,9 @@ hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStre
 // Largest grid of the block-sparse attention kernel on this plan's device, and
 // the work-unit table capacities for that grid.
 int k64_sparse_grid_cap(const tra_plan_s& p);
-void split_capacities(int grid_cap, int rows, int head_dim, int* units_cap, int* splits_cap, int* slots_cap);
+void split_capacities(int grid_cap, int rows, int NB, int head_dim, int* units_cap, int* splits_cap,
+                      int* slots_cap);
+constexpr int kUnitHdrInts = 16;  // header of the work-unit tables
 hipError_t launch_attention_f32(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
 
 hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32_t* budget,
