@@ -55,10 +55,13 @@
  * void*, NULL = the null stream), checks its arguments before launching, and
  * returns a status.  The caller owns every buffer -- tensors and workspaces
  * -- and keeps it alive until the stream has drained.  The plan owns only its
- * device tables (permutation, thresholds, block boxes, per-position counts at
- * the largest radius, key-block distance words); no call writes them, so a
- * plan is immutable after creation and may be shared by calls on any number
- * of streams at once.
+ * device tables (permutation, thresholds, block boxes, key-block distance
+ * words, and the count lookup table of App. C.1: C(n) for every candidate
+ * radius at every position of one octant of the grid, ceil(F/2) ceil(H/2)
+ * ceil(W/2) (n_cap + 1) ints -- 331 MB at 21 x 45 x 80 -- or, where that
+ * would exceed 1 GiB, C(n_cap) per position); no call writes them, so a plan
+ * is immutable after creation and may be shared by calls on any number of
+ * streams at once.
  *
  * Calls that need scratch device memory take it from the caller as
  * (workspace, workspace_bytes): a device buffer, 256-byte aligned, of at least
@@ -233,7 +236,7 @@ tra_status tra_entropy(tra_plan plan, const void* q, const void* k, const void* 
                        void* stream);
 
 /* Entropy -> budget -> squared radius, per token (Sec. 3.1-3.2; App. C.1,
- * Eq. implementation-budget-radius).
+ * Eq. implementation-budget-radius: a bisection over the plan's count table).
  * For a video token, K_hat is evaluated in fp64 by the plan's mapping and
  * clamped to [1, S]:
  *   UNIFORM    K_hat = ceil(tau * exp(H));

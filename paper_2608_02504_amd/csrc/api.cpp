@@ -183,6 +183,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_thr1);
   (void)hipFree(p->d_blocks);
   (void)hipFree(p->d_cap_count);
+  (void)hipFree(p->d_ctab);
   (void)hipFree(p->d_kinfo);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
@@ -255,9 +256,24 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       return fail(TRA_ERR_ALLOC, std::string("plan table upload: ") + hipGetErrorString(e));
     }
     if (!tiles) p->d_perma = p->d_perm;
-    if ((e = hipMalloc((void**)&p->d_cap_count, (size_t)std::max(p->N, 1) * sizeof(int32_t))) != hipSuccess ||
-        (e = tra::fill_cap_counts(*p, p->d_cap_count, nullptr)) != hipSuccess ||
-        (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
+    // App. C.1's count table where it fits the size limit, else C(n_cap) per position
+    const size_t ctab_bytes = tra::count_table_bytes(*p);
+    if (ctab_bytes <= tra::kCountTableMaxBytes) {
+      int32_t* disk_tmp = nullptr;
+      const size_t disk_bytes = (size_t)((cfg->height + 1) / 2) * ((cfg->width + 1) / 2) * ((size_t)p->n_cap + 1) *
+                                sizeof(int32_t);
+      if ((e = hipMalloc((void**)&p->d_ctab, ctab_bytes)) != hipSuccess ||
+          (e = hipMalloc((void**)&disk_tmp, disk_bytes)) != hipSuccess ||
+          (e = tra::fill_count_table(*p, p->d_ctab, disk_tmp, nullptr)) != hipSuccess ||
+          (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
+        (void)hipFree(disk_tmp);
+        tra_plan_destroy(p);
+        return fail(TRA_ERR_ALLOC, std::string("plan count table: ") + hipGetErrorString(e));
+      }
+      (void)hipFree(disk_tmp);
+    } else if ((e = hipMalloc((void**)&p->d_cap_count, (size_t)std::max(p->N, 1) * sizeof(int32_t))) != hipSuccess ||
+               (e = tra::fill_cap_counts(*p, p->d_cap_count, nullptr)) != hipSuccess ||
+               (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
       tra_plan_destroy(p);
       return fail(TRA_ERR_ALLOC, std::string("plan count table: ") + hipGetErrorString(e));
     }

@@ -74,7 +74,11 @@ struct tra_plan_s {
   int32_t* d_thr = nullptr;
   int32_t* d_thr1 = nullptr;  // 1-D thresholds (TRA_DIST_1D plans only)
   int32_t* d_blocks = nullptr;
-  int32_t* d_cap_count = nullptr;  // [N] C(n_cap) per video position (raster)
+  // C(n) of every candidate radius over one octant of the grid (App. C.1's
+  // lookup table), or NULL above kCountTableMaxBytes; then d_cap_count holds
+  // C(n_cap) per video position (raster) and the other counts run on the fly
+  int32_t* d_ctab = nullptr;
+  int32_t* d_cap_count = nullptr;
   // Per-call device memory.  The pointers below marked "call workspace" are
   // NULL in a stored plan, which no call writes; each call works on a copy of
   // the plan with them pointing into the caller's workspace buffer.
@@ -143,6 +147,11 @@ hipError_t launch_budget_radius(const tra_plan_s& p, const float* entropy, int32
                                 int32_t* radius_sq, hipStream_t s);
 // Fills the plan's per-position table of C(n_cap) (once, at plan creation).
 hipError_t fill_cap_counts(const tra_plan_s& p, int32_t* out, hipStream_t s);
+// The count table of App. C.1 over one octant of the grid: its size, and its
+// fill (disk_tmp: ceil(H/2) ceil(W/2) (n_cap + 1) ints of scratch).
+constexpr size_t kCountTableMaxBytes = (size_t)1 << 30;
+size_t count_table_bytes(const tra_plan_s& p);
+hipError_t fill_count_table(const tra_plan_s& p, int32_t* ctab, int32_t* disk_tmp, hipStream_t s);
 
 hipError_t launch_block_mask(const tra_plan_s& p, const int32_t* radius_sq, uint8_t* mask,
                              int32_t* cnt, int32_t* cols, hipStream_t s);
