@@ -140,7 +140,6 @@ typedef enum { TRA_DIST_2D = 0, TRA_DIST_1D = 1 } tra_distance;
  *   tile_w) + ceil(T / b).  A block then has the smallest spatial footprint b
  *   tokens can have, so fewer of its keys lie outside a query's radius: App. D
  *   names that in-block work as the block-granular method's main limitation.
- *   bf16 plans only.
  * tra_entropy and tra_dense_attention are defined over tokens and give the
  * same results under both layouts. */
 typedef enum { TRA_BLOCKS_PACKED = 0, TRA_BLOCKS_TILES = 1 } tra_block_layout;

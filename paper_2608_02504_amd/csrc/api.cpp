@@ -329,6 +329,7 @@ static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a, vo
     bound.n_pad = p->n_pada;
     bound.rows = p->rowsa;
     bound.d_perm = p->d_perma;
+    bound.d_bcount = nullptr;  // packed: every block full but the last
   }
   hipError_t e = p->cfg.dtype == TRA_BF16
                      ? tra::launch_attention_bf16(bound, a, (hipStream_t)stream)

@@ -29,6 +29,7 @@ struct F32Params {
   const int32_t* cnt;
   const int32_t* cols;
   const int32_t* order;
+  const int32_t* bcount;  // tokens of each block (tile-aligned layout), NULL: packed
   int N, NB, rows;
   float alpha;
   // token-level attention only
@@ -70,8 +71,9 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
   const int bh = r / P.NB, u = r - bh * P.NB;
   const int t = threadIdx.x;
   const int qpos = u * B + t;
-  const bool qvalid = qpos < P.N;
-  const int qrow = qvalid ? P.perm[qpos] : 0;
+  const int qtok = P.perm[qpos];  // -1 at a padding position
+  const bool qvalid = qtok >= 0;
+  const int qrow = qvalid ? qtok : 0;
   const size_t head_off = (size_t)bh * P.N * D;
 
   float qr[D];
@@ -84,7 +86,7 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
   // token mask: a text query (or a FULL radius) covers every key
   int n_i = 0;
   bool all_keys = true;
-  if (TOK && qvalid && qpos < P.Nv) {
+  if (TOK && qvalid && qrow < P.Nv) {
     n_i = P.radius_sq[(size_t)bh * P.N + qrow];
     all_keys = n_i > P.n_cap;
     n_i = max(n_i, 0);
@@ -94,7 +96,7 @@ __global__ __launch_bounds__(B) void attn_f32_kernel(F32Params P) {
   for (int c = 0; c < count; ++c) {
     const int vb = SPARSE ? P.cols[(size_t)r * P.NB + c] : c;
     if (vb < 0 || vb >= P.NB) continue;  // uniform across the workgroup
-    const int nv = min(B, P.N - vb * B);
+    const int nv = P.bcount ? P.bcount[vb] : min(B, P.N - vb * B);  // a block's tokens fill its first positions
     for (int j0 = 0; j0 < nv; j0 += kSub) {
       const int ns = min(kSub, nv - j0);
       __syncthreads();
@@ -161,7 +163,8 @@ template <int D, int B>
 hipError_t launch_f32_db(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   const bool one_d = p.cfg.distance == TRA_DIST_1D;
   F32Params P{(const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.o, a.lse,
-              a.entropy, p.d_perm, a.cnt, a.cols, a.order, p.S, p.NB, p.rows,
+              a.entropy, p.d_perm, a.cnt, a.cols, a.order,
+              a.sparse && p.cfg.block_layout == TRA_BLOCKS_TILES ? p.d_bcount : nullptr, p.S, p.NB, p.rows,
               1.0f / sqrtf((float)D), a.radius_sq, one_d ? p.d_thr1 : p.d_thr, p.N,
               p.cfg.frames, p.cfg.height, p.cfg.width, p.n_cap};
   const dim3 grid(p.rows), block(B);

@@ -48,7 +48,6 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   if (c.block_layout != TRA_BLOCKS_PACKED && c.block_layout != TRA_BLOCKS_TILES) { *why = "unknown block layout"; return TRA_ERR_INVALID_ARG; }
   if (c.block_layout == TRA_BLOCKS_TILES) {
     if ((int64_t)c.tile_h * c.tile_w != c.block) { *why = "tile-aligned blocks need tile_h * tile_w == block"; return TRA_ERR_INVALID_ARG; }
-    if (c.dtype != TRA_BF16) { *why = "tile-aligned blocks are supported on bf16 plans only"; return TRA_ERR_UNSUPPORTED; }
   }
   const int64_t n = (int64_t)c.frames * c.height * c.width + c.text_tokens;
   const int64_t nb = c.block_layout == TRA_BLOCKS_TILES

@@ -168,7 +168,6 @@ int main() {
   tra_config b6 = good[1]; b6.text_tokens = -1; bad.push_back(b6);
   tra_config b7 = good[1]; b7.distance = 7; bad.push_back(b7);
   tra_config b8 = good[1]; b8.block_layout = TRA_BLOCKS_TILES; b8.tile_w = 8; bad.push_back(b8);
-  tra_config b9 = good[0]; b9.block_layout = TRA_BLOCKS_TILES; bad.push_back(b9);  // fp32
   for (size_t i = 0; i < bad.size(); ++i) {
     std::string why;
     expect(tra::validate_config(&bad[i], &why) != TRA_OK && !why.empty(), "invalid config accepted",

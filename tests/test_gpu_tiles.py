@@ -11,8 +11,8 @@ import pytest
 
 import oracle as O
 import synth
-from _pipeline import (TOL_O_BF16, OracleTables, Run, check_head, check_lists, log, retained_fraction,
-                       sample_blocks)
+from _pipeline import (TOL_O_BF16, TOL_O_FP32, OracleTables, Run, check_head, check_lists, log,
+                       retained_fraction, sample_blocks)
 
 pytestmark = pytest.mark.gpu
 
@@ -39,13 +39,23 @@ W = {
 }
 W["joint_bf16_d128"] = W["ragged_bf16_d128"].replace(name="joint_bf16_d128", text_tokens=77)
 W["joint_bf16_d64"] = W["ragged_bf16_d64"].replace(name="joint_bf16_d64", text_tokens=200)
+# fp32 plans (the correctness path): 8 x 16 tiles over 7 x 19 frames (clipped
+# tiles of 112, 56 and 21 tokens), and 8 x 8 tiles with b = 64 over 9 x 11
+W["ragged_fp32_d128"] = synth.Workload("ragged_fp32_d128", 1, 2, 128, "fp32", 3, 7, 19, 128,
+                                       0.25, 4.0, 0.6, seed=77, tile_h=8, tile_w=16)
+W["fp32_b64_d64_text"] = synth.Workload("fp32_b64_d64_text", 1, 2, 64, "fp32", 2, 9, 11, 64,
+                                        0.25, 4.0, 0.6, seed=82, tile_h=8, tile_w=8, text_tokens=50)
+
+
+def _tol(w):
+    return TOL_O_BF16 if w.dtype == "bf16" else TOL_O_FP32
 
 
 def _full(run, tabs, report):
     w = run.w
     for b in range(w.batch):
         for h in range(w.heads):
-            check_head(run, tabs, b, h, np.arange(tabs.n_blocks), TOL_O_BF16, report)
+            check_head(run, tabs, b, h, np.arange(tabs.n_blocks), _tol(w), report)
     check_lists(run)
     assert report["near_integer_budgets"] == 0
 
@@ -66,7 +76,8 @@ def test_tiles_full_parity(name, rule, radius):
     log(f"{name} tiles {rule} radius {radius}: NB {tabs.n_blocks} rho={retained_fraction(run, tabs):.4f} {report}")
 
 
-@pytest.mark.parametrize("name", ["ragged_bf16_d128", "joint_bf16_d128", "small_frames_bf16"])
+@pytest.mark.parametrize("name", ["ragged_bf16_d128", "joint_bf16_d128", "small_frames_bf16",
+                                  "ragged_fp32_d128", "fp32_b64_d64_text"])
 @pytest.mark.parametrize("radius", [0, 3, 40])
 def test_tiles_token_attention(name, radius):
     """Token-level attention on tile-aligned blocks against the oracle's
@@ -91,7 +102,7 @@ def test_tiles_token_attention(name, radius):
                 q, k, v, tabs.perm, w.block, list(range(tabs.n_blocks)), M, run.rad[b, h].cpu().numpy(),
                 tabs.F, tabs.H, tabs.W, w.gamma, return_lse=True)
             err = np.abs(o[b, h].double().cpu().numpy()[rows] - o_ref).max()
-            assert err <= TOL_O_BF16, f"token attention max-abs {err:.3e} (b={b}, h={h})"
+            assert err <= _tol(w), f"token attention max-abs {err:.3e} (b={b}, h={h})"
             lse_gpu = lse[b, h].double().cpu().numpy()[rows]
             assert np.abs(lse_gpu - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "token lse"
             worst = max(worst, float(err))

@@ -100,7 +100,6 @@ def test_tiny_layout_sizes():
     (dict(distance="3d"), 1), (dict(text_tokens=-1), 1),
     (dict(text_tokens=4096 * 128), 2),   # more than 4096 blocks
     (dict(block_layout="tiles", tile_h=8, tile_w=8), 1),           # a tile must hold one block
-    (dict(block_layout="tiles", dtype="fp32", block=64, tile_h=8, tile_w=8), 2),  # bf16 only
     (dict(block_layout="diag"), 1),
 ])
 def test_invalid_configs_rejected(change, status):
