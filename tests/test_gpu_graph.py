@@ -27,12 +27,12 @@ W = {
 }
 
 
-@pytest.mark.parametrize("name", list(W))
-def test_graph_replays_match_eager(name):
+@pytest.mark.parametrize("name,layout", [(n, "packed") for n in W] + [("ragged_bf16_d128", "tiles")])
+def test_graph_replays_match_eager(name, layout):
     _gpu()
     import torch
     import paper_2608_02504_amd as tra
-    run = Run(W[name], radius_override=40)        # partial lists
+    run = Run(W[name], radius_override=40, block_layout=layout)   # partial lists
     outs = {k: torch.empty_like(run.O_sp) for k in ("sp", "d", "tok", "ent_o")}
     lse = {k: torch.empty_like(run.lse_sp) for k in ("sp", "d", "tok")}
     H = torch.empty_like(run.H)
@@ -68,4 +68,4 @@ def test_graph_replays_match_eager(name):
         got = {k: v for k, v in list(outs.items()) + [("lse_" + k, v) for k, v in lse.items()] + [("H", H)]}
         for k in eager:
             assert torch.equal(got[k], eager[k]), (rep, k)
-        log(f"{name}: replay {rep} equals the eager calls")
+        log(f"{name} ({layout}): replay {rep} equals the eager calls")
