@@ -25,7 +25,11 @@
 //   is persistent: as many workgroups as can be resident, each taking rows
 //   from a row queue (per-XCD contiguous ranges with stealing, see next_row)
 //   until it is drained.  Several workgroups share a CU, so a SIMD can run one
-//   workgroup's matrix phase while another is in its softmax.
+//   workgroup's matrix phase while another is in its softmax.  Block-sparse
+//   calls take work units instead of rows: long rows are cut into pieces whose
+//   partial results a merge kernel combines, and each XCD's segment of the
+//   unit table lists its split pieces first, piece-major, so that the
+//   workgroups of one XCD walk the same key range (see plan_units_kernel).
 //
 // Per tile (split barriers)
 //   K and V^T go from HBM straight into LDS (global_load_lds_dwordx4 from a
