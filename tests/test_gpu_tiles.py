@@ -79,15 +79,16 @@ def test_tiles_full_parity(name, rule, radius):
 @pytest.mark.parametrize("name", ["ragged_bf16_d128", "joint_bf16_d128", "small_frames_bf16",
                                   "ragged_fp32_d128", "fp32_b64_d64_text"])
 @pytest.mark.parametrize("radius", [0, 3, 40])
-def test_tiles_token_attention(name, radius):
+@pytest.mark.parametrize("distance", ["2d", "1d"])
+def test_tiles_token_attention(name, radius, distance):
     """Token-level attention on tile-aligned blocks against the oracle's
     token_attention_rows over the padded order (union lists, so Eq. 16 over all
-    keys)."""
+    keys), with the 2-D distance and the 1-D ablation."""
     _gpu()
     import torch
     import paper_2608_02504_amd as tra
     w = W[name]
-    run = Run(w, rule="union", radius_override=radius, block_layout="tiles")
+    run = Run(w, rule="union", radius_override=radius, block_layout="tiles", distance=distance)
     tabs = OracleTables(w, block_layout="tiles")
     o = torch.empty_like(run.q)
     lse = torch.empty_like(run.lse_sp)
@@ -100,13 +101,13 @@ def test_tiles_token_attention(name, radius):
             M = run.mask[b, h].cpu().numpy().astype(bool)
             rows, o_ref, lse_ref = O.token_attention_rows(
                 q, k, v, tabs.perm, w.block, list(range(tabs.n_blocks)), M, run.rad[b, h].cpu().numpy(),
-                tabs.F, tabs.H, tabs.W, w.gamma, return_lse=True)
+                tabs.F, tabs.H, tabs.W, w.gamma, distance=distance, return_lse=True)
             err = np.abs(o[b, h].double().cpu().numpy()[rows] - o_ref).max()
             assert err <= _tol(w), f"token attention max-abs {err:.3e} (b={b}, h={h})"
             lse_gpu = lse[b, h].double().cpu().numpy()[rows]
             assert np.abs(lse_gpu - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "token lse"
             worst = max(worst, float(err))
-    log(f"{name} tiles token radius {radius}: max-abs {worst:.2e}")
+    log(f"{name} tiles token {distance} radius {radius}: max-abs {worst:.2e}")
 
 
 def test_tiles_equal_packed_when_tiles_divide_the_frame():
