@@ -75,7 +75,9 @@
  *     bytes, rewritten by every call, plus 512 bytes of row-queue counters
  *     that the call resets and draws its query-block rows from;
  *   tra_sparse_attention, in addition: the work-unit tables and the split
- *     rows' partial results (at most 256 MiB, see that call);
+ *     rows' partial results, (head_dim + 3) x 512 bytes for each of up to
+ *     32 G + 1 pieces (G the workgroups the GPU holds at once; 1.65 GB at
+ *     head_dim 128 on MI355X, less where the plan has fewer blocks);
  *   tra_build_block_mask with a non-NULL order: the counting-sort histograms
  *     of the row order, 4 x ((NB + 1) x ceil(batch x heads x NB / 256) + 1)
  *     bytes (the only workspace of fp32 plans; with a NULL order the mask call
@@ -292,9 +294,7 @@ tra_status tra_build_block_mask_noalloc(tra_plan plan, const int32_t* radius_sq,
  * retained keys, or NULL.  A row with cnt = 0 gets o = 0, lse = -inf.
  * Work is balanced by cutting long lists: with T the total of the (clamped)
  * list lengths of the rows computed and G the number of workgroups the GPU
- * holds at once, a row of more than L = max(48, ceil(T / 16G)) entries (L
- * doubled while the pieces would not fit the 256 MiB of partial results the
- * workspace holds)
+ * holds at once, a row of more than L = max(48, ceil(T / 16G)) entries
  * is computed as ceil(cnt / L) pieces of consecutive entries whose partial
  * softmax states are merged afterwards, so its result differs from an
  * unsplit computation by rounding only (each piece rounds its probabilities

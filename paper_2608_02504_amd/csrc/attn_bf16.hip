@@ -1271,8 +1271,9 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 
 // Work units of a block-sparse call (one workgroup of 1024 threads).  With T
 // the total list length and G the attention grid, L = max(kSplitMin, ceil(T /
-// (G kSplitPerWG))), doubled until the pieces fit the workspace's partial
-// slots, and a row of c > L entries becomes ceil(c / L) units of near-equal
+// (G kSplitPerWG))) (doubled while the pieces would exceed the workspace's
+// partial slots, which its capacity, 2 G kSplitPerWG + 1 slots, rules out),
+// and a row of c > L entries becomes ceil(c / L) units of near-equal
 // length, each writing a partial slot, so that no unit holds more than about
 // 1 / kSplitPerWG of a workgroup's share of the work and the rows the call
 // waits on at its end are short, while short rows are never cut into pieces
@@ -1297,7 +1298,6 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // ceil(NB / kSplitMin) slots / 2): the call's workspace holds tables of these
 // bounds (entries past a capacity are never written).
 constexpr int kSplitPerWG = 16;
-constexpr long long kSplitSlotBytes = 256ll << 20;  // partial results in a call's workspace
 constexpr int kSplitMin = 48;
 
 __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restrict__ cnt,
@@ -1878,9 +1878,11 @@ int k64_sparse_grid_cap(const tra_plan_s& p) {
 
 void split_capacities(int grid_cap, int rows, int NB, int head_dim, int* units_cap, int* splits_cap,
                       int* slots_cap) {
+  (void)head_dim;
   const long long share = (long long)grid_cap * kSplitPerWG;
-  const long long slot_bytes = (long long)kBQ * (head_dim + 3) * 4;
-  *slots_cap = (int)std::min<long long>(2 * share + 1, kSplitSlotBytes / slot_bytes);
+  // a split row of c entries has fewer than 2 c / L pieces, and L >= T / share,
+  // L >= kSplitMin: at most 2 share pieces, and at most 2 rows ceil(NB / kSplitMin)
+  *slots_cap = (int)std::min<long long>(2 * share + 1, 2LL * rows * ((NB + kSplitMin - 1) / kSplitMin) + 1);
   *splits_cap = (int)std::min<long long>(INT_MAX, share + 1);
   // piece-major segments: at most ceil(NB / kSplitMin) units per split row,
   // and at most slots / 2 split rows
