@@ -1293,7 +1293,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 //
 // Writes units[U] = {row, list begin, list end, slot or -1} (row -1: a
 // placeholder), splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L,
-// 0, segment starts x 9}.  A split row has c / L < pieces < 2 c / L, so P <= T
+// 0, segment starts x 9}, and zeroes the attention kernel's queue counters.  A split row has c / L < pieces < 2 c / L, so P <= T
 // / L <= G kSplitPerWG; with the placeholders U <= rows + max(G kSplitPerWG,
 // ceil(NB / kSplitMin) slots / 2): the call's workspace holds tables of these
 // bounds (entries past a capacity are never written).
@@ -1304,12 +1304,14 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
                                                           const int32_t* __restrict__ order, int rows, int NB,
                                                           int n_wg, int4* __restrict__ units, int units_cap,
                                                           int4* __restrict__ splits, int splits_cap,
-                                                          int slots_cap, int32_t* __restrict__ hdr) {
+                                                          int slots_cap, int32_t* __restrict__ hdr,
+                                                          int32_t* __restrict__ ctr) {
   __shared__ long long s_red[1024];
   __shared__ int s_scan[3][1024];
   __shared__ int s_seg[4][1024];  // per thread, segmented: split rows, other rows, max pieces
   __shared__ int s_base[9];
   const int t = threadIdx.x;
+  if (t < kRowCounters) ctr[t] = 0;  // the attention kernel's queue counters, zeroed here for it
   const bool segmented = order == nullptr;
   // this thread's positions [k0, k1) of the walk: in segment t / 128 for the
   // per-XCD queues, else 1/1024 of the caller's order
@@ -1567,9 +1569,11 @@ void launch_k64_lse(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   if (SPARSE) {
     grid = std::min(grid, p.split_wg_cap);
     hipLaunchKernelGGL(plan_units_kernel, dim3(1), dim3(1024), 0, s, a.cnt, a.order, p.rows, p.NB, grid,
-                       (int4*)p.d_units, p.units_cap, (int4*)p.d_splits, p.splits_cap, p.slots_cap, p.d_unit_hdr);
+                       (int4*)p.d_units, p.units_cap, (int4*)p.d_splits, p.splits_cap, p.slots_cap, p.d_unit_hdr,
+                       p.d_row_ctr);
+  } else {
+    hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   }
-  hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE, LSE>), dim3(grid), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cols,
                      p.cfg.block_layout == TRA_BLOCKS_TILES ? p.d_bcount : nullptr, (const int4*)p.d_units,
