@@ -101,55 +101,62 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // ------------------------------------------------------------ layout pre-pass
+// Both gathers take (batch, head) pairs bh = blockIdx.y, blockIdx.y + gridDim.y, ...
+// (the grid's y extent is capped at kGatherMaxY).
+constexpr int kGatherMaxY = 65535;
+
 // kt[bh][p][:] = k[bh][perm[p]][:], 0 where perm[p] < 0 (a padding position).
-__global__ __launch_bounds__(256) void gather_k_kernel(const uint4* __restrict__ k,
-                                                       uint4* __restrict__ kt,
-                                                       const int32_t* __restrict__ perm, int N,
-                                                       int n_pad, int ch, long long total) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= total) return;
-  const long long per_head = (long long)n_pad * ch;
-  const long long bh = idx / per_head;
-  const long long rem = idx - bh * per_head;
-  const int p = (int)(rem / ch), c = (int)(rem - (long long)p * ch);
+// Grid: (16-byte chunks of one head / 256, pairs); thread = one chunk.
+template <int D>
+__global__ __launch_bounds__(256) void gather_k_kernel(const uint4* __restrict__ k, uint4* __restrict__ kt,
+                                                       const int32_t* __restrict__ perm, int N, int n_pad,
+                                                       int bhs) {
+  constexpr int CH = D / 8;
+  const int idx = blockIdx.x * 256 + threadIdx.x;  // < n_pad * CH < 2^24
+  if (idx >= n_pad * CH) return;
+  const int p = idx / CH, c = idx % CH;
   const int tok = perm[p];
-  kt[idx] = tok >= 0 ? k[(bh * N + tok) * ch + c] : make_uint4(0, 0, 0, 0);
+  for (size_t bh = blockIdx.y; bh < (size_t)bhs; bh += gridDim.y)
+    kt[bh * n_pad * CH + idx] = tok >= 0 ? k[(bh * N + tok) * CH + c] : make_uint4(0, 0, 0, 0);
 }
 
 // V transposed per key block, tile-major: for tile-major position p = 128 b + j,
 // vt[bh][b][d][j] = v[bh][perm[p]][d] (0 at a padding position), so key block b of a
 // head is one contiguous D x 128 tile with the key index fastest.  One
-// workgroup per 64 tokens of one head, through LDS.
+// workgroup per 64 positions (of one pair at a time), through LDS.
 template <int D>
 __global__ __launch_bounds__(256) void gather_vt_kernel(const uint16_t* __restrict__ v,
                                                         uint16_t* __restrict__ vt,
                                                         const int32_t* __restrict__ perm, int N,
-                                                        int n_pad) {
+                                                        int n_pad, int bhs) {
   constexpr int TOK = 64, CH = D / 8, LS = D + 2;
   __shared__ uint16_t tile[TOK * LS];
-  const int bh = blockIdx.y, p0 = blockIdx.x * TOK, t = threadIdx.x;
-  for (int i = t; i < TOK * CH; i += 256) {
-    const int j = i / CH, c = i - j * CH;
-    uint4 x = make_uint4(0, 0, 0, 0);
-    const int tok = perm[p0 + j];
-    if (tok >= 0) x = *(const uint4*)(v + ((size_t)bh * N + tok) * D + c * 8);
-    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  const int p0 = blockIdx.x * TOK, t = threadIdx.x;
+  for (int bh = blockIdx.y; bh < bhs; bh += gridDim.y) {
+    __syncthreads();  // the previous pair's reads of the tile are done
+    for (int i = t; i < TOK * CH; i += 256) {
+      const int j = i / CH, c = i - j * CH;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      const int tok = perm[p0 + j];
+      if (tok >= 0) x = *(const uint4*)(v + ((size_t)bh * N + tok) * D + c * 8);
+      const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      tile[j * LS + c * 8 + 2 * e] = (uint16_t)(w[e] & 0xFFFFu);
-      tile[j * LS + c * 8 + 2 * e + 1] = (uint16_t)(w[e] >> 16);
+      for (int e = 0; e < 4; ++e) {
+        tile[j * LS + c * 8 + 2 * e] = (uint16_t)(w[e] & 0xFFFFu);
+        tile[j * LS + c * 8 + 2 * e + 1] = (uint16_t)(w[e] >> 16);
+      }
     }
-  }
-  __syncthreads();
-  for (int i = t; i < D * (TOK / 8); i += 256) {
-    const int d = i / (TOK / 8), tc = i - d * (TOK / 8);
-    uint32_t w[4];
+    __syncthreads();
+    for (int i = t; i < D * (TOK / 8); i += 256) {
+      const int d = i / (TOK / 8), tc = i - d * (TOK / 8);
+      uint32_t w[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      w[e] = (uint32_t)tile[(tc * 8 + 2 * e) * LS + d] | ((uint32_t)tile[(tc * 8 + 2 * e + 1) * LS + d] << 16);
-    const int p = p0 + tc * 8;
-    *(uint4*)(vt + (size_t)bh * n_pad * D + ((size_t)(p / kBK) * D + d) * kBK + p % kBK) =
-        make_uint4(w[0], w[1], w[2], w[3]);
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)tile[(tc * 8 + 2 * e) * LS + d] | ((uint32_t)tile[(tc * 8 + 2 * e + 1) * LS + d] << 16);
+      const int p = p0 + tc * 8;
+      *(uint4*)(vt + (size_t)bh * n_pad * D + ((size_t)(p / kBK) * D + d) * kBK + p % kBK) =
+          make_uint4(w[0], w[1], w[2], w[3]);
+    }
   }
 }
 
@@ -338,6 +345,18 @@ constexpr float kMaxFloor = -1.0e20f;
 // normalisation by l at the end is unchanged, and the O rescale -- and with it
 // most of the max bookkeeping -- runs on the first tiles of a row only.
 constexpr float kMaxSlack = 8.0f;
+
+// In the 128-key kernel (entropy pass, token-level attention), tiles after a
+// wave's first take their weights against the current reference
+// without forming the tile max: a lane's sum of weights at most kFastSum bounds
+// every weight by it (they are positive), so nothing can overflow -- weights up
+// to 2^20 keep O, l and the bf16 probabilities far inside the fp32 / bf16
+// range for any |v| below 2^80.  Only when some lane's sum exceeds it (or is
+// not finite) is the tile redone from its max, which moves the reference; on
+// the method's inputs that is a fraction of a percent of the tiles.  The
+// reference is always some earlier tile's max, so the largest weight of a row
+// is at least 1 and nothing that matters underflows.
+constexpr float kFastSum = 1048576.0f;  // 2^20
 
 // New exponent reference of one query from its tile max (log2 units).
 __device__ __forceinline__ float next_reference(float m, float tile_max_scaled) {
@@ -781,6 +800,7 @@ __device__ __forceinline__ void bf16_row(
   int b_cur;
   int i = next_valid(0, &b_cur);
   int parity = 0;
+  bool fresh = true;  // no tile of the row done by this wave yet
   if (i < count) {
     b_cur = __builtin_amdgcn_readfirstlane(b_cur);
     issue_tile<D>(k_lds, Kb + b_cur * kTileBytes, k_off);
@@ -844,12 +864,20 @@ __device__ __forceinline__ void bf16_row(
           }
         }
         if (n_keys < kBK) mask_tail(s, n_keys, half);
-        sc = tile_max<ENT>(s, scale_log2, st);
         float lsum = 0.f, asum = 0.f, lrsum = 0.f;
+        bool exact = fresh;
+        if (!exact) {  // weights against the current reference (kFastSum)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+          for (int kt = 0; kt < 4; ++kt) tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+          exact = __ballot(!((PV ? lrsum : lsum) <= kFastSum)) != 0;
         }
+        if (exact) {  // the wave's first tile, or a weight past 2^20: from the tile max
+          sc = tile_max<ENT>(s, scale_log2, st);
+          lsum = asum = lrsum = 0.f;
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt) tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+        }
+        fresh = false;
         st.l += lsum;
         if (PV) st.lr += lrsum;
         if (ENT) st.a += asum;
@@ -1116,6 +1144,10 @@ __device__ __forceinline__ void k64_row(
             s[kt][e] = __uint_as_float(((__float_as_uint(s[kt][e]) & keep) | (neg & ~keep)));
           }
       }
+      // (the tile max is always formed here: skipping it as the 128-key
+      // kernel does keeps the score tile live through the exponentials, and at
+      // this kernel's 168 registers the compiler then keeps one LDS read in
+      // flight instead of four -- 2-8 % slower)
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
@@ -1299,6 +1331,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // bounds (entries past a capacity are never written).
 constexpr int kSplitPerWG = 16;
 constexpr int kSplitMin = 48;
+constexpr int kPlanStagedRows = 32768;  // rows whose lengths plan_units_kernel keeps in LDS (64 KB)
 
 __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restrict__ cnt,
                                                           const int32_t* __restrict__ order, int rows, int NB,
@@ -1310,9 +1343,18 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
   __shared__ int s_scan[3][1024];
   __shared__ int s_seg[4][1024];  // per thread, segmented: split rows, other rows, max pieces
   __shared__ int s_base[9];
+  __shared__ uint16_t s_len[kPlanStagedRows];  // the row lengths, read once with coalesced loads
   const int t = threadIdx.x;
   if (t < kRowCounters) ctr[t] = 0;  // the attention kernel's queue counters, zeroed here for it
   const bool segmented = order == nullptr;
+  // (each thread's walk below is a contiguous range of rows, which would read
+  // the counts with one dependent-latency load per row in every pass)
+  const bool staged = rows <= kPlanStagedRows;
+  if (staged) {
+#pragma unroll 8
+    for (int r = t; r < rows; r += 1024) s_len[r] = (uint16_t)min(max(cnt[r], 0), NB);
+    __syncthreads();
+  }
   // this thread's positions [k0, k1) of the walk: in segment t / 128 for the
   // per-XCD queues, else 1/1024 of the caller's order
   int k0, k1;
@@ -1328,7 +1370,9 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
     k1 = min(rows, k0 + per);
   }
   auto row_at = [&](int k) { return order ? order[k] : k; };
-  auto len_of = [&](int r) { return (r >= 0 && r < rows) ? min(max(cnt[r], 0), NB) : -1; };
+  auto len_of = [&](int r) {
+    return (r >= 0 && r < rows) ? (staged ? (int)s_len[r] : min(max(cnt[r], 0), NB)) : -1;
+  };
   long long tot = 0;
   for (int k = k0; k < k1; ++k) tot += max(len_of(row_at(k)), 0);
   s_red[t] = tot;
@@ -1429,7 +1473,7 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
       for (int s = 0; s < p_most; ++s) {
         int4 un = make_int4(-1, 0, 0, -1);
         if (s < pieces && fits)
-          un = make_int4(r, (int)((long long)c * s / pieces), (int)((long long)c * (s + 1) / pieces), sb + s);
+          un = make_int4(r, c * s / pieces, c * (s + 1) / pieces, sb + s);  // c s < 2^24: 32-bit
         const int pos = base + s * n_split + ks;
         if (pos < units_cap) units[pos] = un;
       }
@@ -1457,7 +1501,7 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
     // unit and its other entries become placeholders the kernel skips)
     const bool split = pieces > 1 && sb + pieces <= slots_cap && pb < splits_cap;
     for (int s = 0; s < pieces; ++s) {
-      const int b0 = (int)((long long)c * s / pieces), b1 = (int)((long long)c * (s + 1) / pieces);
+      const int b0 = c * s / pieces, b1 = c * (s + 1) / pieces;  // c s < 2^24: 32-bit
       int4 un = make_int4(r, b0, b1, split ? sb + s : -1);
       if (!split && pieces > 1) un = s == 0 ? make_int4(r, 0, c, -1) : make_int4(-1, 0, 0, -1);
       if (ub + s < units_cap) units[ub + s] = un;
@@ -1849,16 +1893,15 @@ void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
 
 template <int D>
 hipError_t launch_bf16_d(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
-  const int ch = D / 8;
   const int bhs = p.cfg.batch * p.cfg.heads;
-  const long long total = (long long)bhs * p.n_pad * ch;
-  hipLaunchKernelGGL(gather_k_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     (const uint4*)a.k, (uint4*)p.d_kt, p.d_perm, p.S, p.n_pad, ch, total);
+  const unsigned gy = (unsigned)std::min(bhs, kGatherMaxY);
+  hipLaunchKernelGGL((gather_k_kernel<D>), dim3((unsigned)((p.n_pad * (D / 8) + 255) / 256), gy), dim3(256), 0, s,
+                     (const uint4*)a.k, (uint4*)p.d_kt, p.d_perm, p.S, p.n_pad, bhs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.v) {
-    hipLaunchKernelGGL((gather_vt_kernel<D>), dim3(p.n_pad / 64, bhs), dim3(256), 0, s,
-                       (const uint16_t*)a.v, p.d_vt, p.d_perm, p.S, p.n_pad);
+    hipLaunchKernelGGL((gather_vt_kernel<D>), dim3(p.n_pad / 64, gy), dim3(256), 0, s,
+                       (const uint16_t*)a.v, p.d_vt, p.d_perm, p.S, p.n_pad, bhs);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
