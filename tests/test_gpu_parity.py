@@ -10,8 +10,8 @@ import pytest
 
 import oracle as O
 import synth
-from _pipeline import (TOL_O_BF16, TOL_O_FP32, OracleTables, Run, check_head, check_lists, log,
-                       retained_fraction, sample_blocks, to_np_f64)
+from _pipeline import (TOL_H_ABS, TOL_H_REL, TOL_O_BF16, TOL_O_FP32, OracleTables, Run, check_head, check_lists,
+                       dense_reference, log, retained_fraction, sample_blocks, to_np_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -274,6 +274,57 @@ def test_entropy_closed_forms(dtype):
     Hn = H.cpu().numpy()
     assert np.abs(Hn[0, 0] - math.log(N)).max() < 1e-4 * math.log(N)
     assert np.abs(Hn[0, 1]).max() < 1e-4
+
+
+def test_scores_jumping_in_late_tiles():
+    """Scores that rise block by block along the tile-major order (0, 5, 15,
+    35 nats plus a small spread): after the first tile the entropy and token
+    kernels take weights against the reference without a tile max, accept the
+    +5 nat tile (weights up to 2^7.2) and redo the +15 and +35 nat tiles from
+    their max (weights past 2^20).  Entropy-only, fused entropy + output,
+    dense and token-level (full radius, every block listed) results against
+    the oracle (Eq. 2, Eq. 1)."""
+    _gpu()
+    import torch
+    import paper_2608_02504_amd as tra
+    w = synth.Workload("jumps", 1, 2, 128, "bf16", 2, 12, 20, 128, 0.25, 4.0, 0.6, tile_h=8, tile_w=16)
+    plan = tra.Plan(tra.Config.from_workload(w))
+    N, d = w.n_tokens, w.head_dim
+    perm = O.tile_major_order(w.frames, w.height, w.width, w.tile_h, w.tile_w)
+    rng = np.random.default_rng(5)
+    level = np.array([0.0, 5.0, 15.0, 35.0])[np.arange(N) // 128]   # by tile-major position
+    q = np.zeros((2, N, d), np.float32)
+    k = rng.standard_normal((2, N, d)).astype(np.float32) * 0.5
+    v = rng.standard_normal((2, N, d)).astype(np.float32)
+    q[:, :, 0] = 1.0
+    q[1, :, 0] = rng.uniform(0.5, 1.0, N)                 # per-query temperature on head 1
+    k[:, perm, 0] = (level + 0.3 * rng.uniform(0, 1, N)) * math.sqrt(d)
+    qb, kb, vb = (synth.bf16_bits_from_f32(a) for a in (q, k, v))
+    dev = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).reshape(1, 2, N, d).cuda()
+    qt, kt, vt = dev(qb), dev(kb), dev(vb)
+    H = torch.empty(1, 2, N, device="cuda")
+    Hf = torch.empty_like(H)
+    Of, Od, Ot = (torch.empty_like(qt) for _ in range(3))
+    tra.tra_entropy(plan, qt, kt, None, None, H)
+    tra.tra_entropy(plan, qt, kt, vt, Of, Hf)
+    tra.tra_dense_attention(plan, qt, kt, vt, Od)
+    NB = plan.n_blocks
+    rad = torch.full((1, 2, N), tra.TRA_RADIUS_FULL, dtype=torch.int32, device="cuda")
+    cnt = torch.full((1, 2, NB), NB, dtype=torch.int32, device="cuda")
+    cols = torch.arange(NB, dtype=torch.int32, device="cuda").repeat(1, 2, NB, 1)
+    tra.tra_token_attention(plan, qt, kt, vt, rad, cnt, cols, None, Ot)
+    torch.cuda.synchronize()
+    for h in range(2):
+        q64, k64, v64 = (synth.to_f64(a[h], "bf16") for a in (qb, kb, vb))
+        H_ref, O_ref, _ = dense_reference(q64, k64, v64, np.arange(N))
+        tol = np.maximum(TOL_H_REL * np.abs(H_ref), TOL_H_ABS)
+        for name, got in (("entropy", H), ("fused entropy", Hf)):
+            dH = np.abs(got[0, h].double().cpu().numpy() - H_ref)
+            assert (dH <= tol).all(), f"{name} head {h}: max |dH| {dH.max():.3e}"
+        for name, got in (("fused output", Of), ("dense", Od), ("token-level", Ot)):
+            err = np.abs(got[0, h].double().cpu().numpy() - O_ref).max()
+            assert err <= TOL_O_BF16, f"{name} head {h}: max-abs {err:.3e}"
+        log(f"score jumps head {h}: H in [{H_ref.min():.3f}, {H_ref.max():.3f}] nats, all within the bars")
 
 
 def _close_to_rounding(a, b):
