@@ -423,6 +423,10 @@ def joint_driver(tra, w, iters=3):
     return res
 
 
+REFRESH_KEYS = ("per_step_ms", "refresh_step_ms", "reuse_step_ms", "retained_fraction_last_mask",
+                "mask_drift_hamming_mean", "mask_drift_jaccard_mean")
+
+
 def reuse_driver(tra, w, steps=50, refresh=5, seed_offset=100, target_rho=None, on_step=None):
     """Warm-up reuse sequence: step 0 from the generator, later steps drift
     q, k <- q, k + 0.02 N(0,1) (fp32 masters, re-rounded).  Every `refresh`
@@ -828,6 +832,14 @@ def main():
         log("warm-up reuse sequence with entropies shifted to keep ~15 % of the blocks")
         out["reuse_sequence_at_paper_density"] = reuse_driver(tra, rw, steps=args.reuse_steps,
                                                               target_rho=0.15)
+        # the refresh interval (App. B.1 compares refreshing every 10, 5 and 2
+        # steps with never refreshing after warm-up): per-step time and drift
+        log("refresh intervals 2 / 10 / never at the same density")
+        ivals = {"5": {k: out["reuse_sequence_at_paper_density"][k] for k in REFRESH_KEYS}}
+        for r in (2, 10, args.reuse_steps):
+            res = reuse_driver(tra, rw, steps=args.reuse_steps, refresh=r, target_rho=0.15)
+            ivals["never" if r >= args.reuse_steps else str(r)] = {k: res[k] for k in REFRESH_KEYS}
+        out["reuse_refresh_intervals"] = ivals
     if not args.no_cpu:
         log(f"cpu baseline: oracle on a bounded sample (~{args.cpu_seconds:.0f} s)")
         out["cpu_baseline"] = cpu_baseline(w, q_np, k_np, v_np, args.cpu_seconds, src)
