@@ -185,6 +185,7 @@ tra_status tra_plan_destroy(tra_plan p) {
   (void)hipFree(p->d_cap_count);
   (void)hipFree(p->d_ctab);
   (void)hipFree(p->d_kinfo);
+  (void)hipFree(p->d_kfeat);
   if (prev >= 0) (void)hipSetDevice(prev);
   delete p;
   return ok();
@@ -281,6 +282,14 @@ tra_status tra_plan_create(const tra_config* cfg, tra_plan* out) {
       if ((e = upload(&p->d_kinfo, t.kinfo)) != hipSuccess) {
         tra_plan_destroy(p);
         return fail(TRA_ERR_ALLOC, std::string("plan key-info table: ") + hipGetErrorString(e));
+      }
+      if (!t.kfeat.empty()) {
+        const size_t bytes = t.kfeat.size() * sizeof(uint16_t);
+        if ((e = hipMalloc((void**)&p->d_kfeat, bytes)) != hipSuccess ||
+            (e = hipMemcpy(p->d_kfeat, t.kfeat.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess) {
+          tra_plan_destroy(p);
+          return fail(TRA_ERR_ALLOC, std::string("plan key-feature table: ") + hipGetErrorString(e));
+        }
       }
       p->split_wg_cap = tra::k64_sparse_grid_cap(*p);
       tra::split_capacities(p->split_wg_cap, p->rows, p->NB, cfg->head_dim, &p->units_cap, &p->splits_cap,

@@ -429,6 +429,7 @@ struct TokArgs {
   const int32_t* kinfo;      // [NB][kKeyInfo] key distance words, then frames
   const int32_t* binfo;      // [NB][kBlockInfo] block boxes
   const int32_t* coord;      // [S] packed (f, x, y) per tile-major position
+  const uint16_t* kfeat;     // 2-D: [NB][128][kKeyFeat] f16 key vectors of the token mask
   int Nv, F, n_cap;
 };
 
@@ -486,6 +487,40 @@ __device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restr
         }
       }
     }
+}
+
+// 2-D token mask of one score tile as a matrix product: E^T = B_K A_Q^T on a
+// 32x32x8 f16 MFMA per 32-key sub-tile, with the keys' vectors b_j (8 f16
+// integers each, from the plan's key-feature table, rows in the same krow
+// order as the K operand so that E lines up with S element by element) and
+// this lane's query vector a_i, so that E_ij = T_i(frame of j) - D_ij (1 for a
+// text key).  The key is covered iff E_ij >= 0; every term is an integer and
+// every partial sum stays below 2^24, so the test is exact.  Lane half h holds
+// components 4h..4h+3 of both vectors: a_i = (h_lo, l_lo, h_hi, l_hi | 2048, 1,
+// 2x_i, 2y_i) with T - x_i^2 - y_i^2 = 2048 h + l for the thresholds of the
+// block's first and second frame (a query covering every key gets T = 2^22,
+// beyond any squared distance on a 1023 x 1023 frame).
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void token_mask_mfma(f32x16 (&s)[4], const lds_u8* __restrict__ kfeat, int krow,
+                                                int half, int qw, int t_lo, int t_hi) {
+  const int qx = qw & 0xFFFF, qy = qw >> 16;
+  const int sq = qx * qx + qy * qy;
+  const int a_lo = min(t_lo, 1 << 22) - sq, a_hi = min(t_hi, 1 << 22) - sq;
+  const f16x4 qa = {(_Float16)(half ? 2048 : a_lo >> 11), (_Float16)(half ? 1 : a_lo & 2047),
+                    (_Float16)(half ? 2 * qx : a_hi >> 11), (_Float16)(half ? 2 * qy : a_hi & 2047)};
+  const uint32_t neg = __float_as_uint(-1.0e30f);
+  f32x16 zero;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) zero[e] = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    const uint32_t off = ((32 * kt + krow) * kKeyFeat + 4 * half) * 2;
+    const f16x4 ka = __builtin_bit_cast(f16x4, *(const __attribute__((address_space(3))) uint2*)(kfeat + off));
+    const f32x16 e = __builtin_amdgcn_mfma_f32_32x32x8f16(ka, qa, zero, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[kt][i] = e[i] >= 0.f ? s[kt][i] : __uint_as_float(neg);
+  }
 }
 
 // Row queue of the persistent attention kernels (thread 0 of a workgroup only).  Without a
@@ -792,9 +827,18 @@ __device__ __forceinline__ void bf16_row(
   // token variant: wave 0 copies each tile's key info (1 KB) right after its
   // K steps, into the buffer of the tile's parity, so "K landed" covers it
   [[maybe_unused]] const uint32_t kinfo_lds = (uint32_t)(uintptr_t)smemKinfo;
+  // per tile: 2-D the key vectors (2 KB, two copies), 1-D the key words (one 1 KB copy)
+  constexpr int kKeyBufBytes = (TOK & 3) == 1 ? kBK * kKeyFeat * 2 : 1024;
+  constexpr int kKeyCopies = (TOK & 3) == 1 ? 2 : 1;
   auto issue_kinfo = [&](int b, int parity) {
-    if constexpr (TOK != 0) {
-      if (wave == 0) dma16<0>((const uint8_t*)(tk.kinfo + (size_t)b * kKeyInfo), lane * 16, kinfo_lds + parity * 1024);
+    if constexpr ((TOK & 3) == 1) {  // 2-D: the block's 128 key vectors, 2 KB
+      if (wave == 0) {
+        const uint8_t* src = (const uint8_t*)(tk.kfeat + (size_t)b * kBK * kKeyFeat);
+        dma16<0>(src, lane * 16, kinfo_lds + parity * kKeyBufBytes);
+        dma16<1024>(src + 1024, lane * 16, kinfo_lds + parity * kKeyBufBytes);
+      }
+    } else if constexpr (TOK != 0) {
+      if (wave == 0) dma16<0>((const uint8_t*)(tk.kinfo + (size_t)b * kKeyInfo), lane * 16, kinfo_lds + parity * kKeyBufBytes);
     }
   };
   int b_cur;
@@ -859,8 +903,9 @@ __device__ __forceinline__ void bf16_row(
       if (!wave_skip) {
         if constexpr (TOK != 0) {
           if (wave_test) {
-            const lds_u8* ki = (const lds_u8*)smemKinfo + parity * 1024;
-            token_mask<TOK>(s, ki, half, tq_word, t_lo, t_hi);
+            const lds_u8* ki = (const lds_u8*)smemKinfo + parity * kKeyBufBytes;
+            if constexpr ((TOK & 3) == 1) token_mask_mfma(s, ki, krow, half, tq_word, t_lo, t_hi);
+            else token_mask<TOK>(s, ki, half, tq_word, t_lo, t_hi);
           }
         }
         if (n_keys < kBK) mask_tail(s, n_keys, half);
@@ -885,7 +930,7 @@ __device__ __forceinline__ void bf16_row(
       if constexpr (PV) {
         // V_i landed (K_{i+1} -- and for wave 0 of the token variant its key
         // info -- may still be in flight)
-        if (has_next && TOK != 0 && wave == 0) wait_vm<TileCopy<D>::STEPS + 1>();
+        if (has_next && TOK != 0 && wave == 0) wait_vm<TileCopy<D>::STEPS + kKeyCopies>();
         else if (has_next) wait_vm<TileCopy<D>::STEPS>();
         else wait_vm<0>();
         lds_barrier();
@@ -956,7 +1001,7 @@ __global__ __launch_bounds__(kThreads, OCC) void attn_bf16_kernel(
   constexpr int TILE = kBK * D * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t smemK[TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t smemV[PV ? TILE : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t smemKinfo[TOK ? 2 * 1024 : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t smemKinfo[(TOK & 3) == 1 ? 2 * kBK * kKeyFeat * 2 : TOK ? 2 * 1024 : 16];
   extern __shared__ int32_t smemCols[];
   __shared__ int s_row, s_steal;  // thread 0's queue state lives in LDS, not in a register
   if (threadIdx.x == 0) s_steal = 0;
@@ -1883,7 +1928,7 @@ void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   size_t lds_bytes = SPARSE ? (size_t)((p.NB + 3) & ~3) * sizeof(int32_t) : 0;
   if (TOK != 0) lds_bytes += (size_t)kBQ * p.cfg.frames * sizeof(uint16_t);
   const TokArgs tk{a.radius_sq, p.cfg.distance == TRA_DIST_1D ? p.d_thr1 : p.d_thr, p.d_kinfo, p.d_blocks,
-                   p.d_coord, p.N, p.cfg.frames, p.n_cap};
+                   p.d_coord, p.d_kfeat, p.N, p.cfg.frames, p.n_cap};
   const int grid = resident_grid(attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>, lds_bytes, p);
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>), dim3(grid), dim3(kThreads), lds_bytes, s,

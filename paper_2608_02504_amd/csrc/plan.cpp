@@ -64,6 +64,16 @@ tra_status validate_config(const tra_config* cfg, std::string* why) {
   return TRA_OK;
 }
 
+uint16_t f16_bits_of_int(int v) {
+  if (v == 0) return 0;
+  const uint16_t sign = v < 0 ? 0x8000 : 0;
+  unsigned a = (unsigned)(v < 0 ? -v : v);  // 1 .. 2048
+  int e = 0;
+  while ((a >> (e + 1)) != 0) ++e;           // a = 1.m x 2^e, e <= 11
+  const unsigned mant = ((a << 10) >> e) & 0x3FF;
+  return (uint16_t)(sign | ((unsigned)(e + 15) << 10) | mant);
+}
+
 double normal_quantile(double p) {
   // Phi(x) = erfc(-x / sqrt 2) / 2 is increasing; bisect until the bracket
   // stops shrinking in fp64.
@@ -198,6 +208,42 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
           word = 1u << 31;
         }
         t->kinfo[(size_t)u * kKeyInfo + j] = (int32_t)word;
+      }
+    }
+    if (!one_d) {
+      // key side of the token mask as a matrix product (Eq. 15): with the
+      // squared radius thresholds T_lo, T_hi of a query i for the block's
+      // first and second frame, A = T - (x_i^2 + y_i^2) split as 2048 h + l
+      // (0 <= l < 2048) and the key's x^2 + y^2 as 2048 hj + lj, the query
+      // vector a_i = (h_lo, l_lo, h_hi, l_hi, 2048, 1, 2 x_i, 2 y_i) and the key
+      // vector b_j = (2048, 1, 0, 0, -hj, -lj, x_j, y_j) (first frame; (0, 0,
+      // 2048, 1, ...) in the second) give a_i . b_j = T - (x_i - x_j)^2 -
+      // (y_i - y_j)^2, so the key is covered iff it is >= 0.  Every entry is an
+      // integer of magnitude <= 2048, exact in f16, and every partial sum stays
+      // below 2^24, exact in fp32.  A text key is (0, 0, 0, 0, 0, 1, 0, 0)
+      // (a . b = 1, always covered); padding is 0.
+      t->kfeat.assign((size_t)t->NB * b * kKeyFeat, 0);
+      for (int u = 0; u < t->NB; ++u) {
+        const int first = u * b < t->P ? perm[(size_t)u * b] : -1;
+        const int f0 = first >= 0 && first < t->N ? first / (H * W) : 0;
+        for (int j = 0; j < b; ++j) {
+          const int p = u * b + j;
+          const int i = p < t->P ? perm[p] : -1;
+          int v[kKeyFeat] = {0, 0, 0, 0, 0, 0, 0, 0};
+          if (i >= 0 && i < t->N) {
+            const int x = (i / W) % H, y = i % W, sq = x * x + y * y;
+            const int o = i / (H * W) != f0 ? 2 : 0;
+            v[o] = 2048;
+            v[o + 1] = 1;
+            v[4] = -(sq >> 11);
+            v[5] = -(sq & 2047);
+            v[6] = x;
+            v[7] = y;
+          } else if (i >= t->N) {
+            v[5] = 1;
+          }
+          for (int k = 0; k < kKeyFeat; ++k) t->kfeat[((size_t)u * b + j) * kKeyFeat + k] = f16_bits_of_int(v[k]);
+        }
       }
     }
   }

@@ -23,6 +23,7 @@ __host__ __device__ inline int coord_y(int32_t c) { return c & 1023; }
 // per block: f_min f_max x_min x_max y_min y_max n_video r_min r_max n_text
 constexpr int kBlockInfo = 10;
 constexpr int kKeyInfo = 128;  // ints per key block in the key-info table
+constexpr int kKeyFeat = 8;    // f16 values per key in the key-feature table (2-D token mask)
 constexpr int kMaxFrames = 64;
 constexpr int kMaxBlocks = 4096;
 constexpr int kSortChunk = 256;
@@ -39,7 +40,11 @@ struct HostTables {
   std::vector<int32_t> thr1;    // [(n_cap + 1) * F] 1-D thresholds
   std::vector<int32_t> blocks;  // [NB * kBlockInfo]
   std::vector<int32_t> kinfo;   // [(NB + 1) * kKeyInfo]
+  std::vector<uint16_t> kfeat;  // 2-D distance: [NB * block * kKeyFeat] f16 bit patterns
 };
+
+// f16 bit pattern of an integer v with |v| <= 2048 (exact).
+uint16_t f16_bits_of_int(int v);
 
 // Phi^{-1}(p) of the standard normal in fp64, by bisection on Phi.
 double normal_quantile(double p);
@@ -95,6 +100,10 @@ struct tra_plan_s {
   // raster index) with a second-frame flag and a text flag, [NB + 1][128],
   // the key side of the token mask inside a tile.
   int32_t* d_kinfo = nullptr;
+  // bf16 plans with the 2-D distance: per key, 8 f16 integers b with
+  // a_i . b_j = T_i(frame of j) - D_ij for the query vector a_i the token
+  // kernel forms per tile, [NB][128][8] (see build_host_tables).
+  uint16_t* d_kfeat = nullptr;
   int32_t thr_max = 0;  // largest entry of the plan's threshold table
   // bf16 plans, call workspace: row-queue counters of the persistent attention
   // kernel (kRowCounters ints, reset by each call on its stream); the CU count

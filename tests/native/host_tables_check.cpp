@@ -4,6 +4,7 @@
 // 64, a single token, clipped tiles) are validated and built, and the tables'
 // invariants checked; invalid configurations must be rejected.  Exit status 0
 // and no sanitizer report mean pass.
+#include <cmath>
 #include <cstdio>
 #include <string>
 #include <vector>
@@ -13,6 +14,14 @@
 namespace {
 
 int failures = 0;
+
+// Value of an f16 bit pattern (normal numbers and zero).
+double f16_value(uint16_t h) {
+  const int e = (h >> 10) & 31, m = h & 1023;
+  if (e == 0 && m == 0) return (h & 0x8000) ? -0.0 : 0.0;
+  const double v = std::ldexp(1.0 + m / 1024.0, e - 15);
+  return (h & 0x8000) ? -v : v;
+}
 
 void expect(bool ok, const char* what, int cfg) {
   if (!ok) {
@@ -110,6 +119,48 @@ int main() {
                                                         : (uint32_t)((i / c.width) % c.height) | ((uint32_t)(i % c.width) << 16);
         const uint32_t flag = c.distance == TRA_DIST_1D ? 1u << 30 : 1u << 15;
         if ((w & ~flag) != base) { expect(false, "key word", ic); break; }
+      }
+      if (c.distance == TRA_DIST_2D) {
+        // key vectors b_j: for a sample of query positions and thresholds, the
+        // product with the query vector a_i (built here from its definition)
+        // equals T - D for a video key of either frame, and 1 for a text key
+        expect(t.kfeat.size() == (size_t)t.NB * c.block * tra::kKeyFeat, "key-feature table size", ic);
+        bool bad = false;
+        for (int u = 0; u < t.NB && !bad; u += 7) {
+          const int i0 = t.perm[(size_t)u * c.block];
+          const int f0 = i0 < N ? i0 / (c.height * c.width) : 0;
+          for (int j = 0; j < c.block && !bad; ++j) {
+            const int p = u * c.block + j;
+            if (p >= S) break;
+            double bv[tra::kKeyFeat];
+            for (int k = 0; k < tra::kKeyFeat; ++k) bv[k] = f16_value(t.kfeat[(size_t)p * tra::kKeyFeat + k]);
+            const int i = t.perm[p];
+            for (int qi = 0; qi < N && !bad; qi += 997) {
+              const int qx = (qi / c.width) % c.height, qy = qi % c.width;
+              for (int T : {0, 1, 37, 4096, 65535, 1 << 22}) {
+                const int T2 = T / 2 + 3;  // a different threshold for the second frame
+                const int a_lo = T - (qx * qx + qy * qy), a_hi = T2 - (qx * qx + qy * qy);
+                const double a[tra::kKeyFeat] = {(double)(a_lo >> 11), (double)(a_lo & 2047), (double)(a_hi >> 11),
+                                                 (double)(a_hi & 2047), 2048.0, 1.0, 2.0 * qx, 2.0 * qy};
+                double e = 0.0;
+                for (int k = 0; k < tra::kKeyFeat; ++k) e += a[k] * bv[k];
+                double want;
+                if (i >= N) {
+                  want = 1.0;
+                } else {
+                  const int x = (i / c.width) % c.height, y = i % c.width;
+                  const int D = (qx - x) * (qx - x) + (qy - y) * (qy - y);
+                  want = (i / (c.height * c.width) != f0 ? T2 : T) - D;
+                }
+                if (e != want) {
+                  expect(false, "key vector product", ic);
+                  bad = true;
+                  break;
+                }
+              }
+            }
+          }
+        }
       }
     }
   }
