@@ -491,8 +491,9 @@ __device__ __forceinline__ void token_mask(f32x16 (&s)[4], const lds_u8* __restr
 
 // 2-D token mask of one score tile as a matrix product: E^T = B_K A_Q^T on a
 // 32x32x8 f16 MFMA per 32-key sub-tile, with the keys' vectors b_j (8 f16
-// integers each, from the plan's key-feature table, rows in the same krow
-// order as the K operand so that E lines up with S element by element) and
+// integers each, from the plan's key-feature table, stored half-major so that
+// a lane half's reads are consecutive; rows in the same krow order as the K
+// operand so that E lines up with S element by element) and
 // this lane's query vector a_i, so that E_ij = T_i(frame of j) - D_ij (1 for a
 // text key).  The key is covered iff E_ij >= 0; every term is an integer and
 // every partial sum stays below 2^24, so the test is exact.  Lane half h holds
@@ -515,7 +516,7 @@ __device__ __forceinline__ void token_mask_mfma(f32x16 (&s)[4], const lds_u8* __
   for (int e = 0; e < 16; ++e) zero[e] = 0.f;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
-    const uint32_t off = ((32 * kt + krow) * kKeyFeat + 4 * half) * 2;
+    const uint32_t off = half * (kBK * 8) + (32 * kt + krow) * 8;  // [half][key][4] f16
     const f16x4 ka = __builtin_bit_cast(f16x4, *(const __attribute__((address_space(3))) uint2*)(kfeat + off));
     const f32x16 e = __builtin_amdgcn_mfma_f32_32x32x8f16(ka, qa, zero, 0, 0, 0);
 #pragma unroll

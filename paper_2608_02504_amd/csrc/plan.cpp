@@ -242,7 +242,10 @@ void build_host_tables(const tra_config& c, HostTables* t, bool with_perm_coord,
           } else if (i >= t->N) {
             v[5] = 1;
           }
-          for (int k = 0; k < kKeyFeat; ++k) t->kfeat[((size_t)u * b + j) * kKeyFeat + k] = f16_bits_of_int(v[k]);
+          // stored half-major, [u][k / 4][j][k % 4]: a wave's lane half h reads
+          // components 4h..4h+3 of 32 keys as 32 consecutive 8-byte words
+          for (int k = 0; k < kKeyFeat; ++k)
+            t->kfeat[(((size_t)u * 2 + k / 4) * b + j) * 4 + k % 4] = f16_bits_of_int(v[k]);
         }
       }
     }

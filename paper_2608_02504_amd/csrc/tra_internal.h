@@ -40,7 +40,7 @@ struct HostTables {
   std::vector<int32_t> thr1;    // [(n_cap + 1) * F] 1-D thresholds
   std::vector<int32_t> blocks;  // [NB * kBlockInfo]
   std::vector<int32_t> kinfo;   // [(NB + 1) * kKeyInfo]
-  std::vector<uint16_t> kfeat;  // 2-D distance: [NB * block * kKeyFeat] f16 bit patterns
+  std::vector<uint16_t> kfeat;  // 2-D distance: [NB][2][block][4] f16 bit patterns (components 4h..4h+3 at h)
 };
 
 // f16 bit pattern of an integer v with |v| <= 2048 (exact).
@@ -102,7 +102,7 @@ struct tra_plan_s {
   int32_t* d_kinfo = nullptr;
   // bf16 plans with the 2-D distance: per key, 8 f16 integers b with
   // a_i . b_j = T_i(frame of j) - D_ij for the query vector a_i the token
-  // kernel forms per tile, [NB][128][8] (see build_host_tables).
+  // kernel forms per tile, [NB][2][128][4] (see build_host_tables).
   uint16_t* d_kfeat = nullptr;
   int32_t thr_max = 0;  // largest entry of the plan's threshold table
   // bf16 plans, call workspace: row-queue counters of the persistent attention

@@ -133,7 +133,8 @@ int main() {
             const int p = u * c.block + j;
             if (p >= S) break;
             double bv[tra::kKeyFeat];
-            for (int k = 0; k < tra::kKeyFeat; ++k) bv[k] = f16_value(t.kfeat[(size_t)p * tra::kKeyFeat + k]);
+            for (int k = 0; k < tra::kKeyFeat; ++k)  // stored [block][k / 4][key][k % 4]
+              bv[k] = f16_value(t.kfeat[(((size_t)u * 2 + k / 4) * c.block + j) * 4 + k % 4]);
             const int i = t.perm[p];
             for (int qi = 0; qi < N && !bad; qi += 997) {
               const int qx = (qi / c.width) % c.height, qy = qi % c.width;
