@@ -166,6 +166,33 @@ def test_token_unsupported_shapes_are_rejected():
             tra.tra_token_attention(plan, x, x, x, rad, cnt, cols, None, torch.empty_like(x))
 
 
+@pytest.mark.parametrize("radius", [3000, 20000])
+def test_token_attention_largest_frame(radius):
+    """The largest frame bf16 token attention takes (thresholds below 65,536:
+    182 x 182, n_cap = 65,522), two frames: the 2-D key test's vectors reach
+    their largest coordinates and thresholds.  Forced radii leave most tiles
+    partially covered; 24 sampled query blocks (the last included) against the
+    oracle's token_attention_rows."""
+    _gpu()
+    w = synth.Workload("frame182_bf16", 1, 1, 64, "bf16", 2, 182, 182, 128, 0.25, 4.0, 0.6, seed=84,
+                       tile_h=8, tile_w=16)
+    run = Run(w, rule="union", radius_override=radius)
+    o, lse = _token_call(run)
+    tabs = OracleTables(w)
+    q, k, v = (synth.to_f64(a[0, 0], w.dtype) for a in (run.q_np, run.k_np, run.v_np))
+    blocks = sample_blocks(w, 24, seed=11)[(0, 0)]
+    M = run.mask[0, 0].cpu().numpy().astype(bool)[blocks]
+    rows, o_ref, lse_ref = O.token_attention_rows(
+        q, k, v, tabs.perm, w.block, list(blocks), M, run.rad[0, 0].cpu().numpy(), tabs.F, tabs.H, tabs.W,
+        w.gamma, distance="2d", return_lse=True)
+    err = np.abs(o[0, 0].double().cpu().numpy()[rows] - o_ref).max()
+    assert err <= TOL_O_BF16, f"token attention max-abs {err:.3e}"
+    lse_gpu = lse[0, 0].double().cpu().numpy()[rows]
+    assert np.abs(lse_gpu - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max(), "token lse"
+    log(f"182 x 182 frames, radius {radius}: kept {run.cnt.float().mean().item():.1f} blocks per row, "
+        f"token attention max-abs {err:.2e}")
+
+
 @pytest.mark.slow
 def test_token_attention_720p_sampled_at_paper_density():
     """Token-level attention at the headline shape with about 15 % of the blocks
