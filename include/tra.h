@@ -56,7 +56,8 @@
  * returns a status.  The caller owns every buffer -- tensors and workspaces
  * -- and keeps it alive until the stream has drained.  The plan owns only its
  * device tables (permutation, thresholds, block boxes, key-block distance
- * words, and the count lookup table of App. C.1: C(n) for every candidate
+ * words and, for the 2-D distance, the per-key vectors of the token-level key
+ * test, and the count lookup table of App. C.1: C(n) for every candidate
  * radius at every position of one octant of the grid, ceil(F/2) ceil(H/2)
  * ceil(W/2) (n_cap + 1) ints -- 331 MB at 21 x 45 x 80 -- or, where that
  * would exceed 1 GiB, C(n_cap) per position); no call writes them, so a plan
@@ -322,7 +323,9 @@ tra_status tra_sparse_attention(tra_plan plan, const void* q, const void* k,
  * tra_sparse_attention; a query's own key is always covered, so a query of a
  * row that lists its own block never has an empty softmax; a query that
  * covers no listed key gets o = 0, lse = -inf.  Whole 128-key tiles that none
- * of a wave's 32 queries covers are skipped.  bf16 plans need every threshold
+ * of a wave's 32 queries covers are skipped.  (bf16, 2-D: the test is
+ * evaluated as an exact integer dot product of per-query and per-key vectors on
+ * the matrix cores; the decisions are the same.)  bf16 plans need every threshold
  * below 65536 (n_cap <= 65535 for 2-D, floor(pi/2 n_cap) <= 65535 for 1-D)
  * and, with the packed layout, at least one block of video tokens per frame
  * (H*W >= block), else TRA_ERR_UNSUPPORTED.  workspace: TRA_CALL_TOKEN. */
