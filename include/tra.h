@@ -216,6 +216,20 @@ tra_status tra_plan_host_tables(const tra_config* cfg, int32_t* perm, int32_t* t
  * depends on the plan only, not on the call's data. */
 tra_status tra_workspace_size(tra_plan plan, int32_t call, size_t* bytes);
 
+/* Kernel timing, for benchmarks (not for calls captured into a graph).
+ * tra_kernel_timing(call, n): the calling thread's next n calls of kind
+ * `call` (TRA_CALL_ENTROPY, TRA_CALL_SPARSE, TRA_CALL_TOKEN or TRA_CALL_DENSE)
+ * record a HIP event pair on their stream around their attention kernel
+ * alone -- not around the layout pre-pass, nor the work-unit and merge kernels
+ * of a block-sparse call.  The n event pairs are created here, on the current
+ * device (calls of plans on another device are not timed), and replace the
+ * thread's earlier ones; n = 0 releases them.  1 <= n <= 4096.
+ * tra_kernel_times(ms, n, got): waits for the recorded calls and writes up to
+ * n kernel times (milliseconds, call order) to ms; *got receives how many
+ * calls were recorded. */
+tra_status tra_kernel_timing(int32_t call, int32_t n);
+tra_status tra_kernel_times(float* ms, int32_t n, int32_t* got);
+
 /* Message describing the last failure on the calling thread ("" if none). */
 const char* tra_last_error(void);
 

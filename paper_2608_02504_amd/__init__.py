@@ -30,7 +30,7 @@ __all__ = [
     "tra_workspace_size", "TRA_BLOCKS_PACKED", "TRA_BLOCKS_TILES", "TRA_CALL_ENTROPY", "TRA_CALL_BLOCK_MASK", "TRA_CALL_SPARSE",
     "TRA_CALL_TOKEN", "TRA_CALL_DENSE", "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
     "tra_sparse_attention", "tra_token_attention", "tra_dense_attention", "tra_version",
-    "EXPORTED_SYMBOLS",
+    "tra_kernel_timing", "tra_kernel_times", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtra.so")
@@ -50,7 +50,7 @@ EXPORTED_SYMBOLS = (
     "tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
     "tra_last_error", "tra_version", "tra_entropy", "tra_budget_radius",
     "tra_build_block_mask", "tra_sparse_attention", "tra_token_attention", "tra_dense_attention",
-    "tra_build_block_mask_noalloc", "tra_workspace_size",
+    "tra_build_block_mask_noalloc", "tra_workspace_size", "tra_kernel_timing", "tra_kernel_times",
 )
 
 _STATUS = {0: "TRA_OK", 1: "TRA_ERR_INVALID_ARG", 2: "TRA_ERR_UNSUPPORTED",
@@ -157,8 +157,10 @@ def lib() -> ctypes.CDLL:
     L.tra_sparse_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, Z, V]
     L.tra_token_attention.argtypes = [P, V, V, V, V, V, V, V, V, V, V, Z, V]
     L.tra_dense_attention.argtypes = [P, V, V, V, V, V, V, Z, V]
+    L.tra_kernel_timing.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    L.tra_kernel_times.argtypes = [V, ctypes.c_int32, V]
     for name in ("tra_plan_create", "tra_plan_destroy", "tra_plan_dims", "tra_plan_host_tables",
-                 "tra_workspace_size",
+                 "tra_workspace_size", "tra_kernel_timing", "tra_kernel_times",
                  "tra_entropy", "tra_budget_radius", "tra_build_block_mask", "tra_build_block_mask_noalloc",
                  "tra_sparse_attention", "tra_token_attention", "tra_dense_attention"):
         getattr(L, name).restype = I
@@ -231,6 +233,20 @@ def tra_workspace_size(plan: Plan, call: int) -> int:
     n = ctypes.c_size_t()
     _check(lib().tra_workspace_size(plan.handle, call, ctypes.byref(n)))
     return n.value
+
+
+def tra_kernel_timing(call: int, n: int) -> None:
+    """Time the attention kernel of the calling thread's next n calls of kind
+    `call` (a TRA_CALL_* value) with HIP events; n = 0 stops."""
+    _check(lib().tra_kernel_timing(call, n))
+
+
+def tra_kernel_times(n: int):
+    """Kernel times (ms, call order) of up to n timed calls, after waiting for them."""
+    ms = (ctypes.c_float * max(n, 1))()
+    got = ctypes.c_int32()
+    _check(lib().tra_kernel_times(ms if n > 0 else None, n, ctypes.byref(got)))
+    return [float(ms[i]) for i in range(min(n, got.value))]
 
 
 def tra_plan_dims(plan: Plan):

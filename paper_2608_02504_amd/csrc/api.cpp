@@ -328,10 +328,72 @@ tra_status tra_plan_dims(tra_plan p, int32_t* n_tokens, int32_t* n_blocks, int32
   return ok();
 }
 
-static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a, void* ws, size_t ws_bytes,
+// Kernel timing state of the calling thread (tra_kernel_timing).  The events
+// are not destroyed at thread exit (the runtime may be gone by then).
+namespace {
+struct KernelTiming {
+  int call = -1, device = -1, used = 0;
+  std::vector<hipEvent_t> start, stop;
+  void release() {
+    for (hipEvent_t e : start) (void)hipEventDestroy(e);
+    for (hipEvent_t e : stop) (void)hipEventDestroy(e);
+    start.clear();
+    stop.clear();
+    call = device = -1;
+    used = 0;
+  }
+};
+thread_local KernelTiming g_timing;
+}  // namespace
+
+tra_status tra_kernel_timing(int32_t call, int32_t n) {
+  if (n < 0 || n > 4096) return fail(TRA_ERR_INVALID_ARG, "n must be in [0, 4096]");
+  if (n > 0 && call != TRA_CALL_ENTROPY && call != TRA_CALL_SPARSE && call != TRA_CALL_TOKEN &&
+      call != TRA_CALL_DENSE)
+    return fail(TRA_ERR_INVALID_ARG, "call must be TRA_CALL_ENTROPY, _SPARSE, _TOKEN or _DENSE");
+  g_timing.release();
+  if (n == 0) return ok();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "tra_kernel_timing: no device");
+  for (int i = 0; i < n; ++i) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if ((e = hipEventCreate(&a)) != hipSuccess || (e = hipEventCreate(&b)) != hipSuccess) {
+      if (a) (void)hipEventDestroy(a);
+      g_timing.release();
+      return hip_fail(e, "tra_kernel_timing: event creation");
+    }
+    g_timing.start.push_back(a);
+    g_timing.stop.push_back(b);
+  }
+  g_timing.call = call;
+  g_timing.device = dev;
+  return ok();
+}
+
+tra_status tra_kernel_times(float* ms, int32_t n, int32_t* got) {
+  if (!got) return fail(TRA_ERR_INVALID_ARG, "got is NULL");
+  if (n > 0 && !ms) return fail(TRA_ERR_INVALID_ARG, "ms is NULL");
+  *got = g_timing.used;
+  for (int i = 0; i < std::min<int>(n, g_timing.used); ++i) {
+    hipError_t e = hipEventSynchronize(g_timing.stop[i]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms[i], g_timing.start[i], g_timing.stop[i]);
+    if (e != hipSuccess) return hip_fail(e, "tra_kernel_times");
+  }
+  return ok();
+}
+
+static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a_in, void* ws, size_t ws_bytes,
                                 void* stream, const char* what) {
   tra_plan_s bound;
   TRA_TRY(bind_workspace(p, call, true, ws, ws_bytes, &bound));
+  tra::AttnArgs a = a_in;
+  const bool timed = g_timing.call == call && g_timing.device == p->device &&
+                     g_timing.used < (int)g_timing.start.size();
+  if (timed) {
+    a.ev_start = g_timing.start[g_timing.used];
+    a.ev_stop = g_timing.stop[g_timing.used];
+  }
   if (call == TRA_CALL_ENTROPY || call == TRA_CALL_DENSE) {
     // defined over tokens: run on the packed order whatever the block layout
     bound.NB = p->NBa;
@@ -343,6 +405,7 @@ static tra_status run_attention(tra_plan p, int call, const tra::AttnArgs& a, vo
   hipError_t e = p->cfg.dtype == TRA_BF16
                      ? tra::launch_attention_bf16(bound, a, (hipStream_t)stream)
                      : tra::launch_attention_f32(bound, a, (hipStream_t)stream);
+  if (timed && e == hipSuccess) ++g_timing.used;
   return launch_result(e, what);
 }
 

@@ -1664,11 +1664,13 @@ void launch_k64_lse(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
   } else {
     hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
   }
+  if (a.ev_start) (void)hipEventRecord(a.ev_start, s);
   hipLaunchKernelGGL((attn_k64_kernel<D, SPARSE, LSE>), dim3(grid), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, p.d_perm, a.cols,
                      p.cfg.block_layout == TRA_BLOCKS_TILES ? p.d_bcount : nullptr, (const int4*)p.d_units,
                      p.d_unit_hdr, a.order != nullptr, p.S, p.n_pad, p.NB, p.rows, scale_log2, p.d_row_ctr,
                      p.d_part, p.d_pstats);
+  if (a.ev_stop) (void)hipEventRecord(a.ev_stop, s);
   if (SPARSE)
     hipLaunchKernelGGL((merge_split_rows_kernel<D, LSE>), dim3(std::max(1, std::min(p.splits_cap, 1024))),
                        dim3(256), 0, s, (const int4*)p.d_splits, p.d_unit_hdr, p.d_part, p.d_pstats,
@@ -1918,9 +1920,11 @@ void launch_fused_entropy_output(const tra_plan_s& p, const AttnArgs& a, hipStre
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const int grid = resident_grid(attn_fused_kernel<D>, 0, p, kFusedThreads);
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  if (a.ev_start) (void)hipEventRecord(a.ev_start, s);
   hipLaunchKernelGGL((attn_fused_kernel<D>), dim3(grid), dim3(kFusedThreads), 0, s, (const uint16_t*)a.q,
                      p.d_kt, p.d_vt, (uint16_t*)a.o, a.entropy, p.d_perm, p.S, p.n_pad, p.NB, p.rows,
                      scale_log2, p.d_row_ctr);
+  if (a.ev_stop) (void)hipEventRecord(a.ev_stop, s);
 }
 
 template <int D, bool SPARSE, bool PV, bool ENT, int TOK = 0>
@@ -1932,9 +1936,11 @@ void launch_variant(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) {
                    p.d_coord, p.d_kfeat, p.N, p.cfg.frames, p.n_cap};
   const int grid = resident_grid(attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>, lds_bytes, p);
   hipLaunchKernelGGL(reset_row_counters, dim3(1), dim3(kRowCounters), 0, s, p.d_row_ctr);
+  if (a.ev_start) (void)hipEventRecord(a.ev_start, s);
   hipLaunchKernelGGL((attn_bf16_kernel<D, SPARSE, PV, ENT, 2, TOK>), dim3(grid), dim3(kThreads), lds_bytes, s,
                      (const uint16_t*)a.q, p.d_kt, p.d_vt, (uint16_t*)a.o, a.lse, a.entropy, p.d_perm,
                      a.cnt, a.cols, a.order, p.S, p.n_pad, p.NB, p.rows, scale_log2, tk, p.d_row_ctr);
+  if (a.ev_stop) (void)hipEventRecord(a.ev_stop, s);
 }
 
 template <int D>

@@ -168,6 +168,7 @@ hipError_t launch_f32_db(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
               1.0f / sqrtf((float)D), a.radius_sq, one_d ? p.d_thr1 : p.d_thr, p.N,
               p.cfg.frames, p.cfg.height, p.cfg.width, p.n_cap};
   const dim3 grid(p.rows), block(B);
+  if (a.ev_start) (void)hipEventRecord(a.ev_start, s);
   if (a.sparse && a.radius_sq && one_d)
     hipLaunchKernelGGL((attn_f32_kernel<D, B, true, true, false, 2>), grid, block, 0, s, P);
   else if (a.sparse && a.radius_sq)
@@ -180,6 +181,7 @@ hipError_t launch_f32_db(const tra_plan_s& p, const AttnArgs& a, hipStream_t s) 
     hipLaunchKernelGGL((attn_f32_kernel<D, B, false, false, true>), grid, block, 0, s, P);
   else
     hipLaunchKernelGGL((attn_f32_kernel<D, B, false, true, false>), grid, block, 0, s, P);
+  if (a.ev_stop) (void)hipEventRecord(a.ev_stop, s);
   return hipGetLastError();
 }
 

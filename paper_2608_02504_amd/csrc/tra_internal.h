@@ -142,6 +142,8 @@ struct AttnArgs {
   const int32_t* order;  // sparse only, may be null
   bool sparse;
   const int32_t* radius_sq = nullptr;  // token-level attention (sparse) only
+  // kernel timing: recorded on the call's stream around the attention kernel
+  hipEvent_t ev_start = nullptr, ev_stop = nullptr;
 };
 hipError_t launch_attention_bf16(const tra_plan_s& p, const AttnArgs& a, hipStream_t s);
 // Largest grid of the block-sparse attention kernel on this plan's device, and

@@ -131,7 +131,13 @@ def test_null_arguments_are_errors_not_crashes():
     assert L.tra_token_attention(None, None, None, None, None, None, None, None, None, None, None, 0,
                                  None) == 1
     assert L.tra_dense_attention(None, None, None, None, None, None, None, 0, None) == 1
+    assert L.tra_kernel_times(None, 0, None) == 1
     assert b"NULL" in L.tra_last_error()
+    assert L.tra_kernel_timing(tra.TRA_CALL_BLOCK_MASK, 1) == 1   # not an attention call
+    assert L.tra_kernel_timing(tra.TRA_CALL_SPARSE, -1) == 1
+    assert L.tra_kernel_timing(tra.TRA_CALL_SPARSE, 5000) == 1
+    assert L.tra_kernel_timing(tra.TRA_CALL_SPARSE, 0) == 0      # stopping needs no device
+    assert tra.tra_kernel_times(4) == []
     assert L.tra_plan_destroy(None) == 0
     assert L.tra_last_error() == b""
 
