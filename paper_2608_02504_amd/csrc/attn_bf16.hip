@@ -1589,6 +1589,7 @@ __global__ __launch_bounds__(256) void merge_split_rows_kernel(const int4* __res
     const int qtok = perm[u * kBQ + qi];  // -1 at a padding position
     if (qtok < 0) continue;
     float m = -INFINITY;
+#pragma unroll 4
     for (int p = 0; p < pieces; ++p) {
       const float* ps = pstats + (size_t)(slot0 + p) * 3 * kBQ;
       if (ps[kBQ + qi] > 0.f) m = fmaxf(m, ps[qi]);
@@ -1597,6 +1598,7 @@ __global__ __launch_bounds__(256) void merge_split_rows_kernel(const int4* __res
 #pragma unroll
     for (int j = 0; j < HD; ++j) acc[j] = 0.f;
     float lr = 0.f, lf = 0.f;
+#pragma unroll 2  // two pieces' loads in flight
     for (int p = 0; p < pieces; ++p) {
       const float* ps = pstats + (size_t)(slot0 + p) * 3 * kBQ;
       const float lrp = ps[kBQ + qi];
