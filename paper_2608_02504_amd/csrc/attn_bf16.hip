@@ -1368,6 +1368,11 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 // Long rows keep most of their lists alike (rows whose queries mostly have
 // the full radius keep every block), so the split pieces a queue's workgroups
 // run side by side walk the same key blocks, and the L2 serves them to all.
+// The last 1 / kTailDiv of a segment's whole rows run longest first (bucketed
+// by length, in no fixed order inside a bucket), so that the units its
+// workgroups finish on are the short ones and few of them wait idle at the end
+// of the call; the rows before them keep row order, whose neighbouring rows
+// share key blocks.  A whole row's result does not depend on where it runs.
 //
 // Writes units[U] = {row, list begin, list end, slot or -1} (row -1: a
 // placeholder), splits[P] = {row, first slot, pieces, 0} and hdr = {U, P, L,
@@ -1378,6 +1383,11 @@ __global__ __launch_bounds__(kThreads, 3) void attn_k64_kernel(
 constexpr int kSplitPerWG = 16;
 constexpr int kSplitMin = 48;
 constexpr int kPlanStagedRows = 32768;  // rows whose lengths plan_units_kernel keeps in LDS (64 KB)
+constexpr int kTailDiv = 8;              // the tail: the last eighth of a segment's whole rows
+constexpr int kTailBins = 256;           // length buckets of the tail's order
+
+// Length bucket of a whole row (0 <= c <= L) in the tail's order.
+__device__ __forceinline__ int tail_bin(int c, int L) { return min(kTailBins - 1, c * kTailBins / (L + 1)); }
 
 __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restrict__ cnt,
                                                           const int32_t* __restrict__ order, int rows, int NB,
@@ -1389,6 +1399,7 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
   __shared__ int s_scan[3][1024];
   __shared__ int s_seg[4][1024];  // per thread, segmented: split rows, other rows, max pieces
   __shared__ int s_base[9];
+  __shared__ int s_tail[8][kTailBins];  // per segment: tail rows per length bucket, then their slots
   __shared__ uint16_t s_len[kPlanStagedRows];  // the row lengths, read once with coalesced loads
   const int t = threadIdx.x;
   if (t < kRowCounters) ctr[t] = 0;  // the attention kernel's queue counters, zeroed here for it
@@ -1503,6 +1514,31 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
     const int x = t >> 7, last = x * 128 + 127;
     const int n_split = s_seg[0][last], p_most = s_seg[2][last];
     const int base = s_base[x];
+    const int n_whole = s_seg[1][last];
+    const int keep = n_whole - n_whole / kTailDiv;  // whole rows of rank >= keep form the tail
+    // the tail's order: rows per length bucket, then each bucket's first slot
+    // counted from the longest bucket down
+    for (int i = t; i < 8 * kTailBins; i += 1024) s_tail[i / kTailBins][i % kTailBins] = 0;
+    __syncthreads();
+    {
+      int kw = s_seg[1][t] - nw;
+      for (int k = k0; k < k1; ++k) {
+        const int c = len_of(row_at(k));
+        if (c < 0 || c > L) continue;
+        if (kw >= keep) atomicAdd(&s_tail[x][tail_bin(c, L)], 1);
+        ++kw;
+      }
+    }
+    __syncthreads();
+    if (t < 8) {
+      int run = 0;
+      for (int b = kTailBins - 1; b >= 0; --b) {
+        const int n = s_tail[t][b];
+        s_tail[t][b] = run;
+        run += n;
+      }
+    }
+    __syncthreads();
     int ks = s_seg[0][t] - np, kw = s_seg[1][t] - nw;  // ranks of this thread's first rows
     for (int k = k0; k < k1; ++k) {
       const int r = row_at(k);
@@ -1510,7 +1546,8 @@ __global__ __launch_bounds__(1024) void plan_units_kernel(const int32_t* __restr
       if (c < 0) continue;
       const int pieces = c > L ? (c + L - 1) / L : 1;
       if (pieces == 1) {
-        const int pos = base + p_most * n_split + kw;
+        const int rank = kw < keep ? kw : keep + atomicAdd(&s_tail[x][tail_bin(c, L)], 1);
+        const int pos = base + p_most * n_split + rank;
         if (pos < units_cap) units[pos] = make_int4(r, 0, c, -1);
         ++kw;
         continue;
