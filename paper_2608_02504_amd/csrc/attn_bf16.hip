@@ -389,9 +389,8 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
 // accumulation chains: one long chain of dot products would stall the wave on
 // their latency); with LF the fp32 weights into lsum.
 template <bool PV, bool ENT, bool LF = true>
-__device__ __forceinline__ void tile_exp(const f32x16& s, float scale_log2, float m, float& lsum,
-                                         float& asum, float& lrsum, uint32_t* pb) {
-  float lr4[4] = {0.f, 0.f, 0.f, 0.f};
+__device__ __forceinline__ void tile_exp_acc(const f32x16& s, float scale_log2, float m, float& lsum,
+                                             float& asum, float (&lr4)[4], uint32_t* pb) {
 #pragma unroll
   for (int e = 0; e < 16; e += 2) {
     const float x0 = fmaf(s[e], scale_log2, -m);
@@ -405,6 +404,13 @@ __device__ __forceinline__ void tile_exp(const f32x16& s, float scale_log2, floa
       lr4[(e >> 1) & 3] = add_bf16_pair(pb[e >> 1], lr4[(e >> 1) & 3]);
     }
   }
+}
+
+template <bool PV, bool ENT, bool LF = true>
+__device__ __forceinline__ void tile_exp(const f32x16& s, float scale_log2, float m, float& lsum,
+                                         float& asum, float& lrsum, uint32_t* pb) {
+  float lr4[4] = {0.f, 0.f, 0.f, 0.f};
+  tile_exp_acc<PV, ENT, LF>(s, scale_log2, m, lsum, asum, lr4, pb);
   if (PV) lrsum += (lr4[0] + lr4[1]) + (lr4[2] + lr4[3]);
 }
 
@@ -1206,12 +1212,15 @@ __device__ __forceinline__ void k64_row(
       st.lr *= sc;
       st.m = m_new;
       uint32_t pb[16];
-      float lsum = 0.f, asum = 0.f, lrsum = 0.f;
+      float lsum = 0.f, asum = 0.f;
+      // the rounded weights' four sum chains run over both sub-tiles, the
+      // first one seeded with the running sum
+      float lr4[4] = {st.lr, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
-        tile_exp<true, false, LSE>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+        tile_exp_acc<true, false, LSE>(s[kt], scale_log2, st.m, lsum, asum, lr4, pb + 8 * kt);
       if (LSE) st.l += lsum;
-      st.lr += lrsum;
+      st.lr = (lr4[0] + lr4[1]) + (lr4[2] + lr4[3]);
       if (has_next) wait_vm<STEPS>();  // V^T landed (the next K tile may still be in flight)
       else wait_vm<0>();
       lds_barrier();
