@@ -918,16 +918,21 @@ __device__ __forceinline__ void bf16_row(
         if (n_keys < kBK) mask_tail(s, n_keys, half);
         float lsum = 0.f, asum = 0.f, lrsum = 0.f;
         bool exact = fresh;
+        // (the rounded weights' four sum chains run over all four sub-tiles)
         if (!exact) {  // weights against the current reference (kFastSum)
+          float lr4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt) tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+          for (int kt = 0; kt < 4; ++kt) tile_exp_acc<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lr4, pb + 8 * kt);
+          if (PV) lrsum = (lr4[0] + lr4[1]) + (lr4[2] + lr4[3]);
           exact = __ballot(!((PV ? lrsum : lsum) <= kFastSum)) != 0;
         }
         if (exact) {  // the wave's first tile, or a weight past 2^20: from the tile max
           sc = tile_max<ENT>(s, scale_log2, st);
-          lsum = asum = lrsum = 0.f;
+          lsum = asum = 0.f;
+          float lr4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt) tile_exp<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lrsum, pb + 8 * kt);
+          for (int kt = 0; kt < 4; ++kt) tile_exp_acc<PV, ENT>(s[kt], scale_log2, st.m, lsum, asum, lr4, pb + 8 * kt);
+          if (PV) lrsum = (lr4[0] + lr4[1]) + (lr4[2] + lr4[3]);
         }
         fresh = false;
         st.l += lsum;
