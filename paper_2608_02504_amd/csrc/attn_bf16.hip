@@ -385,9 +385,11 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[4], float scale_log2
 
 // Weights of sub-tile kt: w = 2^(s alpha log2e - m), summed into l (and w x into
 // a); bf16 pairs into pb[8kt .. 8kt+7].
-// With PV the rounded pairs are also summed into lrsum (four independent
-// accumulation chains: one long chain of dot products would stall the wave on
-// their latency); with LF the fp32 weights into lsum.
+// With PV the rounded pairs are also added to the four accumulation chains
+// lr4, which a caller carries over all sub-tiles of a tile (one long chain of
+// dot products would stall the wave on their latency); with LF the fp32
+// weights into lsum.  tile_exp: the same for one sub-tile, with its own
+// chains, their total added to lrsum.
 template <bool PV, bool ENT, bool LF = true>
 __device__ __forceinline__ void tile_exp_acc(const f32x16& s, float scale_log2, float m, float& lsum,
                                              float& asum, float (&lr4)[4], uint32_t* pb) {
